@@ -1,0 +1,121 @@
+"""The library's split-KV work partition, re-implemented in plain Python integers.
+
+TEST INFRASTRUCTURE ONLY (see ``oracle/__init__``).  The library builds its plan in host
+C++; this file re-derives the same table from the written rule so that the two can be
+compared entry by entry.
+
+Why a partition at all: the paper finds that the longest tenth of trajectories takes
+over half of rollout time (Sec. 2.2, "Long-tailed Rollout") and that stragglers set the
+makespan (Sec. 1).  On one GPU the same imbalance appears inside a decode step: a few
+very long sequences next to many short ones.  The rule below cuts long sequences into
+page-aligned KV ranges so that all compute units stay busy, and merges the pieces by
+their log-sum-exps.  The paper does not describe this step; the rule is the library's.
+
+The rule
+--------
+Inputs: per-sequence KV length L_b (after this step's new tokens), query tokens C_b
+(1 for decode), KV heads Hkv, group size G = Hq / Hkv, and parameters (compute units,
+units per CU, minimum split size in pages, maximum splits, chunk query tile).
+
+1. pages_b = ceil(L_b / 16).
+2. Rows with C_b = 1 are *single* rows; rows with C_b > 1 are *chunk* rows.
+3. W = sum over single rows of pages_b * Hkv; target = num_cus * units_per_cu;
+   chunk = max(min_split_pages, ceil(W / target)) (min_split_pages when W = 0).
+4. A single row is cut into n_b = min(max_splits, max(1, ceil(pages_b / chunk))) splits;
+   split j covers pages [floor(j pages_b / n_b), floor((j+1) pages_b / n_b)), i.e. tokens
+   [16 p0, min(16 p1, L_b)).  An empty sequence gets one empty unit.
+5. A chunk row is cut into query tiles of T tokens (T = q_tile, or 16 * max(1, 16 // G)
+   when q_tile = 0): tile k holds new tokens [kT, min(kT + T, C_b)) and keys
+   [0, P_b + min(kT + T, C_b)), where P_b = L_b - C_b.  Tiles are not split along KV.
+6. Every unit is repeated for each KV head g.
+7. Single units are ordered by descending KV token count, ties by ascending (b, g, j);
+   chunk units by descending (KV tokens x query tokens), ties by ascending (b, g, q_begin).
+   The table lists all single units, then all chunk units.
+8. Single rows with n_b > 1 own n_b partial-result slots per KV head, allotted in
+   ascending (b, g) order: part_base(b, g) = (slots of earlier split rows) + g * n_b.
+   Units with n_b = 1 have part_base = -1.
+
+Each unit is 12 int32 fields, in the order of ``UNIT_FIELDS``.
+"""
+from __future__ import annotations
+
+import dataclasses
+
+UNIT_FIELDS = ("b", "g", "kv_begin", "kv_end", "q_begin", "q_end", "split", "n_splits",
+               "part_base", "row0", "kind", "prior")
+KIND_SINGLE = 0
+KIND_CHUNK = 1
+PAGE = 16
+
+
+@dataclasses.dataclass(frozen=True)
+class PlanParams:
+    num_cus: int = 256
+    units_per_cu: int = 2
+    min_split_pages: int = 32
+    max_splits: int = 64
+    q_tile: int = 0
+
+
+def _ceil_div(a: int, b: int) -> int:
+    return -(-a // b)
+
+
+def plan_ref(seq_lens, q_lens, num_kv_heads: int, group: int, params: PlanParams):
+    """Returns (units: list of 12-tuples, info: dict) following the rule above."""
+    L = [int(x) for x in seq_lens]
+    B = len(L)
+    C = [1] * B if q_lens is None else [int(x) for x in q_lens]
+    Hkv = int(num_kv_heads)
+    pages = [_ceil_div(x, PAGE) for x in L]
+    row0 = [0] * B
+    acc = 0
+    for b in range(B):
+        row0[b] = acc
+        acc += C[b]
+
+    single = [b for b in range(B) if C[b] == 1]
+    chunked = [b for b in range(B) if C[b] > 1]
+
+    W = sum(pages[b] * Hkv for b in single)
+    target = params.num_cus * params.units_per_cu
+    chunk = max(params.min_split_pages, _ceil_div(W, target)) if W > 0 else params.min_split_pages
+    n_split = {}
+    for b in single:
+        n_split[b] = min(params.max_splits, max(1, _ceil_div(pages[b], chunk)))
+
+    part_base = {}
+    slots = 0
+    for b in range(B):
+        if b in n_split and n_split[b] > 1:
+            for g in range(Hkv):
+                part_base[(b, g)] = slots + g * n_split[b]
+            slots += n_split[b] * Hkv
+
+    singles = []
+    for b in single:
+        n = n_split[b]
+        for g in range(Hkv):
+            for j in range(n):
+                p0 = (j * pages[b]) // n
+                p1 = ((j + 1) * pages[b]) // n
+                t0 = PAGE * p0
+                t1 = min(PAGE * p1, L[b])
+                singles.append((b, g, t0, t1, 0, 1, j, n, part_base.get((b, g), -1),
+                                row0[b], KIND_SINGLE, L[b] - 1))
+    singles.sort(key=lambda u: (-(u[3] - u[2]), u[0], u[1], u[6]))
+
+    T = params.q_tile if params.q_tile > 0 else PAGE * max(1, 16 // group)
+    chunks = []
+    for b in chunked:
+        P = L[b] - C[b]
+        for g in range(Hkv):
+            for k in range(_ceil_div(C[b], T)):
+                q0 = k * T
+                q1 = min(q0 + T, C[b])
+                chunks.append((b, g, 0, P + q1, q0, q1, 0, 1, -1, row0[b], KIND_CHUNK, P))
+    chunks.sort(key=lambda u: (-(u[3] - u[2]) * (u[5] - u[4]), u[0], u[1], u[4]))
+
+    info = {"n_single": len(singles), "n_chunk": len(chunks), "n_partial_slots": slots,
+            "chunk_pages": chunk, "q_tile": T, "work_pages": W}
+    return singles + chunks, info

@@ -1,0 +1,98 @@
+"""Planted mistakes in the oracle must fail its pins (mutation check, CPU only).
+
+Each mutant patches one piece of ``oracle.attention`` with a plausible slip (a wrong
+scale, a dropped term, a wrong index, a swapped operand, an off-by-one causal bound) and
+runs pins from ``test_oracle_pins``; every mutant has to be caught by at least one.
+"""
+import numpy as np
+import pytest
+
+import oracle.attention as oa
+import test_oracle_pins as pins
+
+_attend = oa.attend
+_gather = oa.gather_tokens
+
+
+def _scale_squared(q, K, V, s, visible=None):
+    return _attend(q, K, V, s * s, visible)
+
+
+def _lse_without_max(q, K, V, s, visible=None):
+    o, lse = _attend(q, K, V, s, visible)
+    if K.shape[0] == 0:
+        return o, lse
+    z = s * (np.asarray(q) @ np.asarray(K).T)
+    if visible is not None:
+        z = np.where(visible, z, -np.inf)
+    return o, lse - z.max(axis=1)
+
+
+def _values_are_keys(q, K, V, s, visible=None):
+    return _attend(q, K, K, s, visible)
+
+
+def _exclusive_causal(q, K, V, s, visible=None):
+    if visible is not None:
+        visible = np.roll(visible, 1, axis=1)
+        visible[:, 0] = False
+    return _attend(q, K, V, s, visible)
+
+
+def _wrong_kv_head(pages, row, kv_head, n):
+    return _gather(pages, row, (kv_head + 1) % pages.shape[1], n)
+
+
+def _slot_page_swapped(pages, row, kv_head, n):
+    out = np.empty((n, pages.shape[-1]), dtype=np.uint16)
+    for t in range(n):
+        out[t] = pages[int(row[t % 16 if t % 16 < len(row) else 0]), kv_head, (t // 16) % 16]
+    return out
+
+
+def _drops_last_token(pages, row, kv_head, n):
+    if n <= 1:
+        return _gather(pages, row, kv_head, n)
+    g = _gather(pages, row, kv_head, n)
+    g[-1] = g[-2]
+    return g
+
+
+ATTEND_MUTANTS = [_scale_squared, _lse_without_max, _values_are_keys]
+GATHER_MUTANTS = [_wrong_kv_head, _slot_page_swapped, _drops_last_token]
+
+
+def _caught(fn, *args):
+    try:
+        fn(*args)
+    except AssertionError:
+        return True
+    return False
+
+
+@pytest.mark.parametrize("mutant", ATTEND_MUTANTS, ids=lambda f: f.__name__)
+def test_attend_mutants_are_caught(monkeypatch, mutant):
+    monkeypatch.setattr(oa, "attend", mutant)
+    assert _caught(pins.test_decode_matches_torch_sdpa, 8, 2)
+
+
+@pytest.mark.parametrize("mutant", GATHER_MUTANTS, ids=lambda f: f.__name__)
+def test_gather_mutants_are_caught(monkeypatch, mutant):
+    monkeypatch.setattr(oa, "gather_tokens", mutant)
+    assert _caught(pins.test_decode_matches_torch_sdpa, 8, 2)
+
+
+def test_causal_off_by_one_is_caught(monkeypatch):
+    monkeypatch.setattr(oa, "attend", _exclusive_causal)
+    assert _caught(pins.test_append_matches_torch_sdpa_lower_right_causal, 7, 9)
+
+
+def test_merge_sign_slip_is_caught(monkeypatch):
+    real = oa.merge_ref
+
+    def wrong(o_parts, lse_parts):
+        return real(o_parts, -np.asarray(lse_parts))
+
+    import oracle
+    monkeypatch.setattr(oracle, "merge_ref", wrong)
+    assert _caught(pins.test_split_anywhere_then_merge_equals_unsplit, [7, 8, 300])

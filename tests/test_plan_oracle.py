@@ -1,0 +1,125 @@
+"""Pins for the plan oracle: hand-derived tables and the invariants the rule promises."""
+import numpy as np
+import pytest
+
+from oracle.plan import PlanParams, plan_ref, UNIT_FIELDS
+
+F = {name: i for i, name in enumerate(UNIT_FIELDS)}
+
+
+def test_hand_derived_decode_example():
+    # L = [40, 0, 100] -> pages [3, 0, 7]; W = 10, target = 1 * 2 = 2,
+    # chunk = max(2, ceil(10 / 2)) = 5; n = [1, 1, 2].  Sequence 2 splits into pages
+    # [0, 3) and [3, 7), i.e. tokens [0, 48) and [48, 100); its two slots start at 0.
+    units, info = plan_ref([40, 0, 100], None, 1, 4,
+                           PlanParams(num_cus=1, units_per_cu=2, min_split_pages=2, max_splits=8))
+    assert units == [
+        (2, 0, 48, 100, 0, 1, 1, 2, 0, 2, 0, 99),
+        (2, 0, 0, 48, 0, 1, 0, 2, 0, 2, 0, 99),
+        (0, 0, 0, 40, 0, 1, 0, 1, -1, 0, 0, 39),
+        (1, 0, 0, 0, 0, 1, 0, 1, -1, 1, 0, -1),
+    ]
+    assert info["n_partial_slots"] == 2 and info["chunk_pages"] == 5
+
+
+def test_hand_derived_append_example():
+    # L = [10, 100], C = [1, 70], Hkv = 2, G = 8 -> T = 16 * (16 // 8) = 32.
+    # Single row 0: one page, W = 2, target = 4, chunk = 1, n = 1.
+    # Chunk row 1: P = 30, tiles [0,32) [32,64) [64,70) with keys [0,62) [0,94) [0,100);
+    # costs 62*32 = 1984, 94*32 = 3008, 100*6 = 600.
+    units, info = plan_ref([10, 100], [1, 70], 2, 8,
+                           PlanParams(num_cus=4, units_per_cu=1, min_split_pages=1, max_splits=4))
+    assert units == [
+        (0, 0, 0, 10, 0, 1, 0, 1, -1, 0, 0, 9),
+        (0, 1, 0, 10, 0, 1, 0, 1, -1, 0, 0, 9),
+        (1, 0, 0, 94, 32, 64, 0, 1, -1, 1, 1, 30),
+        (1, 1, 0, 94, 32, 64, 0, 1, -1, 1, 1, 30),
+        (1, 0, 0, 62, 0, 32, 0, 1, -1, 1, 1, 30),
+        (1, 1, 0, 62, 0, 32, 0, 1, -1, 1, 1, 30),
+        (1, 0, 0, 100, 64, 70, 0, 1, -1, 1, 1, 30),
+        (1, 1, 0, 100, 64, 70, 0, 1, -1, 1, 1, 30),
+    ]
+    assert info["n_single"] == 2 and info["n_chunk"] == 6 and info["q_tile"] == 32
+
+
+def check_invariants(seq_lens, q_lens, hkv, group, params):
+    units, info = plan_ref(seq_lens, q_lens, hkv, group, params)
+    B = len(seq_lens)
+    C = [1] * B if q_lens is None else list(q_lens)
+    singles = units[:info["n_single"]]
+    chunks = units[info["n_single"]:]
+    assert all(u[F["kind"]] == 0 for u in singles) and all(u[F["kind"]] == 1 for u in chunks)
+    # ordering
+    kv = [u[3] - u[2] for u in singles]
+    assert kv == sorted(kv, reverse=True)
+    cost = [(u[3] - u[2]) * (u[5] - u[4]) for u in chunks]
+    assert cost == sorted(cost, reverse=True)
+    # single rows: splits tile [0, L) exactly, page aligned, non-empty unless L = 0
+    slots = set()
+    for b in range(B):
+        if C[b] != 1:
+            continue
+        for g in range(hkv):
+            us = sorted((u for u in singles if u[0] == b and u[1] == g), key=lambda u: u[6])
+            n = us[0][F["n_splits"]]
+            assert len(us) == n and 1 <= n <= params.max_splits
+            assert [u[6] for u in us] == list(range(n))
+            assert us[0][2] == 0 and us[-1][3] == seq_lens[b]
+            for a, c in zip(us[:-1], us[1:]):
+                assert a[3] == c[2] and c[2] % 16 == 0
+            if seq_lens[b] > 0:
+                assert all(u[3] > u[2] for u in us)
+            for u in us:
+                if n > 1:
+                    s = u[F["part_base"]] + u[6]
+                    assert 0 <= s < info["n_partial_slots"] and s not in slots
+                    slots.add(s)
+                else:
+                    assert u[F["part_base"]] == -1
+    assert len(slots) == info["n_partial_slots"]
+    # chunk rows: tiles cover [0, C) and see keys up to P + q_end
+    row0 = np.concatenate([[0], np.cumsum(C)])
+    for b in range(B):
+        if C[b] == 1:
+            continue
+        for g in range(hkv):
+            us = sorted((u for u in chunks if u[0] == b and u[1] == g), key=lambda u: u[4])
+            assert us[0][4] == 0 and us[-1][5] == C[b]
+            for a, c in zip(us[:-1], us[1:]):
+                assert a[5] == c[4]
+            for u in us:
+                P = seq_lens[b] - C[b]
+                assert u[F["prior"]] == P and u[3] == P + u[5] and u[2] == 0
+                assert u[F["row0"]] == row0[b] and u[5] - u[4] <= info["q_tile"]
+    total = sum(u[3] - u[2] for u in singles)
+    assert total == hkv * sum(seq_lens[b] for b in range(B) if C[b] == 1)
+    return units, info
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_plan_invariants_random(seed):
+    rng = np.random.default_rng(seed)
+    B = int(rng.integers(1, 40))
+    lens = rng.choice([0, 1, 15, 16, 17, 31, 33, 500, 4096, 131072], size=B).tolist()
+    lens += rng.integers(1, 70000, size=3).tolist()
+    params = PlanParams(num_cus=int(rng.integers(1, 300)), units_per_cu=int(rng.integers(1, 4)),
+                        min_split_pages=int(rng.integers(1, 64)), max_splits=int(rng.integers(1, 100)))
+    check_invariants(lens, None, int(rng.choice([1, 2, 8])), 4, params)
+    C = rng.choice([1, 1, 1, 2, 64, 1000], size=len(lens)).tolist()
+    lens2 = [max(L, c) for L, c in zip(lens, C)]
+    check_invariants(lens2, C, 2, int(rng.choice([1, 4, 7, 8, 16])), params)
+
+
+def test_longtail_batch_splits_only_the_tail():
+    from paper_2606_03077_amd import workloads as wl
+    lens, _ = wl.draw_lengths(wl.WORKLOADS["longtail"], np.random.default_rng(26063))
+    units, info = check_invariants(lens.tolist(), None, 8, 4, PlanParams())
+    split_rows = {u[0] for u in units if u[F["n_splits"]] > 1}
+    assert split_rows and all(lens[b] > 16 * info["chunk_pages"] for b in split_rows)
+
+
+def test_straggler_batch_splits_every_row():
+    lens = [98304, 131072, 100000, 120000]
+    units, info = check_invariants(lens, None, 8, 8, PlanParams())
+    assert all(u[F["n_splits"]] >= 8 for u in units)
+    assert len(units) >= 256
