@@ -1,0 +1,245 @@
+/*
+ * libra: ragged paged-KV decode and append attention for MI355X (gfx950).
+ *
+ * The hot path underneath an agentic-RL rollout stage (arXiv 2606.03077): rollout is
+ * autoregressive decoding that the paper calls memory- and bandwidth-bound (Sec. 1;
+ * Sec. 2.1; App. A.1), over trajectories whose lengths are long-tailed (Sec. 2.2) and
+ * grow when tool outputs are appended mid-trajectory (Sec. 1; Sec. 5, Phase 2 and the
+ * migration steps).  The paper's engine keeps a per-request paged KV cache that can be
+ * sharded along attention heads (Sec. 5, Step 2); the library keeps that head axis
+ * separable in its layout.
+ *
+ * Conventions for every entry point
+ * ---------------------------------
+ * - All tensors are borrowed pointers owned by the caller.  "device" pointers must be
+ *   HIP device memory of the current device; "host" pointers are ordinary host memory.
+ * - Handles (libra_kv_layout, libra_plan) are created and destroyed by the library and
+ *   are immutable after creation, except that a plan remembers which workspace its
+ *   tables were last uploaded to.
+ * - Work is enqueued asynchronously on `stream` (a hipStream_t; NULL = the null stream).
+ *   No entry point synchronises the device or allocates device memory, except
+ *   libra_plan_destroy, which waits for its own pending upload.
+ * - Every entry point returns a libra_status; nothing aborts, prints or throws.  On an
+ *   error nothing has been enqueued, and libra_last_error() gives a per-thread message.
+ * - Validation happens on the host before any launch.  Device-side contract violations
+ *   (a block-table entry >= num_pages, a block table shorter than the plan's lengths)
+ *   are undefined behaviour: the library does not read the block table on the host.
+ *
+ * Numerics: bf16 inputs, float32 accumulation, bf16 outputs rounded to nearest even,
+ * log-sum-exp in float32 natural log.  Query head h reads KV head h / G with
+ * G = num_q_heads / num_kv_heads (contiguous groups).
+ */
+#ifndef LIBRA_H_
+#define LIBRA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum libra_status {
+  LIBRA_OK = 0,
+  LIBRA_E_INVAL = 1,        /* bad argument: null pointer, size, inconsistent plan */
+  LIBRA_E_UNSUPPORTED = 2,  /* valid but not implemented: head_dim != 128, G > 16 ... */
+  LIBRA_E_WORKSPACE = 3,    /* workspace smaller than libra_plan_workspace_bytes() */
+  LIBRA_E_HIP = 4,          /* a HIP runtime call or kernel launch failed */
+  LIBRA_E_NOMEM = 5         /* host allocation failed */
+} libra_status;
+
+enum {
+  LIBRA_PAGE_SIZE = 16,     /* tokens per page */
+  LIBRA_HEAD_DIM = 128,     /* channels per head */
+  LIBRA_MAX_GROUP = 16,     /* largest supported num_q_heads / num_kv_heads */
+  LIBRA_UNIT_INTS = 12      /* int32 fields per plan unit */
+};
+
+enum { LIBRA_DTYPE_BF16 = 0 };
+enum { LIBRA_MODE_DECODE = 0, LIBRA_MODE_APPEND = 1 };
+
+typedef struct libra_kv_layout_s* libra_kv_layout;
+typedef struct libra_plan_s* libra_plan;
+
+/* Human-readable name of a status code (static storage). */
+const char* libra_status_string(libra_status status);
+/* Detail of the last error raised on the calling thread ("" if none). */
+const char* libra_last_error(void);
+
+/* ------------------------------------------------------------------------------ */
+/* Paged KV cache layout                                                           */
+/* ------------------------------------------------------------------------------ */
+/*
+ * The cache is two caller-owned device buffers, K and V, each num_pages *
+ * num_kv_heads tiles of 4096 bytes.  Tile (page, g) starts at byte
+ * ((page * num_kv_heads) + g) * 4096 and holds the 16 token slots x 128 channels of
+ * that page for KV head g as bf16, so the head axis stays separable per page (the
+ * paper reshards KV along heads, Sec. 5, Step 2).  Inside a tile the element of
+ * (slot s, channel d) sits at:
+ *
+ *   K: ((d / 8) * 16 + s) * 8 + d % 8
+ *   V: (d / 32) * 512 + ((d % 16) + 16 * (s / 4)) * 8 + ((d / 16) % 2) * 4 + s % 4
+ *
+ * i.e. the order in which a 64-lane wavefront consumes them as matrix-core operands,
+ * so that one 16-byte load per lane reads 1 KiB contiguously.  Callers never address
+ * elements directly: libra_kv_pack_pages / libra_kv_unpack_pages convert whole pages
+ * from / to the logical format, and libra_append_attn writes new tokens.
+ *
+ * Logical page format (used by pack / unpack): [n_pages][num_kv_heads][16][128] bf16,
+ * slot-major.  Token t of sequence b lives in page block_table[b * bt_stride + t / 16],
+ * slot t % 16.
+ */
+typedef struct libra_kv_layout_desc {
+  int64_t num_pages;     /* pages in each of k_cache / v_cache, > 0 */
+  int32_t page_size;     /* must be LIBRA_PAGE_SIZE */
+  int32_t num_kv_heads;  /* > 0 */
+  int32_t head_dim;      /* must be LIBRA_HEAD_DIM */
+  int32_t dtype;         /* must be LIBRA_DTYPE_BF16 */
+  void* k_cache;         /* device, num_pages * num_kv_heads * 4096 bytes */
+  void* v_cache;         /* device, same size */
+} libra_kv_layout_desc;
+
+/* Validates the descriptor and returns a handle (the buffers stay caller-owned). */
+libra_status libra_kv_layout_create(const libra_kv_layout_desc* desc, libra_kv_layout* out);
+void libra_kv_layout_destroy(libra_kv_layout layout);
+
+/* Converts n_pages logical pages (device, [n_pages][Hkv][16][128] bf16) into the
+ * layout's pages [first_page, first_page + n_pages).  k_src / v_src may be NULL to
+ * skip one side.  Source and destination must not overlap. */
+libra_status libra_kv_pack_pages(libra_kv_layout layout, const void* k_src, const void* v_src,
+                                 int64_t first_page, int64_t n_pages, void* stream);
+
+/* Inverse of libra_kv_pack_pages: pages [first_page, first_page + n_pages) to logical
+ * format in k_dst / v_dst (device).  Used to offload or reshard a request's cache. */
+libra_status libra_kv_unpack_pages(libra_kv_layout layout, void* k_dst, void* v_dst,
+                                   int64_t first_page, int64_t n_pages, void* stream);
+
+/* Copies the first seq_len tokens of each sequence out of the paged cache through the
+ * block table: k_out / v_out (device) are [sum_b len_b][Hkv][128] bf16 with sequence b
+ * starting at row cu_seq_lens[b].  cu_seq_lens (device, int32 [batch + 1]) is the
+ * prefix sum of the lengths; max_pages bounds ceil(len_b / 16) and bt_stride >=
+ * max_pages.  Bit-exact: it only moves bytes. */
+libra_status libra_kv_gather(libra_kv_layout layout, const int32_t* block_table, int32_t bt_stride,
+                             const int32_t* cu_seq_lens, int32_t batch, int32_t max_pages,
+                             void* k_out, void* v_out, void* stream);
+
+/* ------------------------------------------------------------------------------ */
+/* Split-KV work plan (host)                                                       */
+/* ------------------------------------------------------------------------------ */
+/*
+ * Partitions one batch step into work units so that a long-tailed batch keeps every
+ * compute unit busy: the paper measures that the longest 10% of trajectories take over
+ * half of rollout time (Sec. 2.2) and that stragglers set the makespan (Sec. 1).  The
+ * paper gives no kernel-level rule; this one is the library's:
+ *
+ * 1. pages_b = ceil(L_b / 16), L_b = KV length after this step's new tokens.
+ * 2. Rows with C_b = 1 query token are single rows, rows with C_b > 1 chunk rows.
+ * 3. W = sum over single rows of pages_b * Hkv; target = num_cus * units_per_cu;
+ *    chunk = max(min_split_pages, ceil(W / target)) (min_split_pages if W = 0).
+ * 4. A single row splits into n_b = min(max_splits, max(1, ceil(pages_b / chunk))) KV
+ *    ranges; split j covers pages [floor(j pages_b / n_b), floor((j+1) pages_b / n_b)),
+ *    i.e. tokens [16 p0, min(16 p1, L_b)).  An empty sequence gets one empty unit.
+ * 5. A chunk row is cut into query tiles of T tokens (T = q_tile, or 16 * max(1, 16 / G)
+ *    if q_tile = 0): tile k holds new tokens [kT, min(kT + T, C_b)) and keys
+ *    [0, P_b + min(kT + T, C_b)), P_b = L_b - C_b.  Tiles are not split along KV.
+ * 6. Every unit is repeated for each KV head g.
+ * 7. Single units come first, by descending KV tokens, ties by ascending (b, g, j);
+ *    then chunk units by descending KV tokens x query tokens, ties by (b, g, q_begin).
+ * 8. Single rows with n_b > 1 own n_b float32 partial-result slots per KV head,
+ *    allotted in ascending (b, g): part_base(b, g) = earlier split rows' slots + g n_b.
+ *
+ * Unit fields (LIBRA_UNIT_INTS int32): b, g, kv_begin, kv_end, q_begin, q_end, split,
+ * n_splits, part_base (-1 if unsplit), row0 (first query row of sequence b),
+ * kind (0 single, 1 chunk), prior (P_b = L_b - C_b).
+ * All arithmetic is exact 64-bit integer arithmetic; the table is deterministic.
+ */
+typedef struct libra_plan_params {
+  int32_t num_cus;          /* compute units; 0 = query the current device */
+  int32_t units_per_cu;     /* default 2 */
+  int32_t min_split_pages;  /* default 32 */
+  int32_t max_splits;       /* default 64 */
+  int32_t q_tile;           /* chunk query tile in tokens; 0 = 16 * max(1, 16 / G) */
+} libra_plan_params;
+
+typedef struct libra_plan_desc {
+  int32_t mode;          /* LIBRA_MODE_DECODE (q_lens must be NULL) or LIBRA_MODE_APPEND */
+  int32_t batch;         /* >= 0 sequences */
+  int32_t num_q_heads;   /* Hq, a multiple of num_kv_heads */
+  int32_t num_kv_heads;  /* Hkv */
+} libra_plan_desc;
+
+typedef struct libra_plan_info {
+  int32_t n_units;          /* total units in the table */
+  int32_t n_single;         /* units handled by the decode kernel */
+  int32_t n_chunk;          /* units handled by the chunk kernel */
+  int32_t n_partial_slots;  /* float32 partial results used by split rows */
+  int64_t chunk_pages;      /* step 3's chunk size */
+  int32_t q_tile;           /* step 5's tile size */
+  int32_t n_rows;           /* query rows (sum C_b) */
+  int32_t n_write_tiles;    /* (sequence, page) pairs an append writes */
+  int32_t num_cus;          /* CUs the plan was cut for */
+} libra_plan_info;
+
+/* Builds the plan from host lengths.  seq_lens_host: int32 [batch], L_b >= 0 (>= C_b
+ * for append).  q_lens_host: int32 [batch], C_b >= 1, for append; NULL for decode.
+ * params may be NULL (defaults).  Pure host code apart from num_cus = 0. */
+libra_status libra_splitkv_plan(const libra_plan_desc* desc, const int32_t* seq_lens_host,
+                                const int32_t* q_lens_host, const libra_plan_params* params,
+                                libra_plan* out);
+/* Host view of the unit table (valid until libra_plan_destroy). */
+libra_status libra_plan_get_units(libra_plan plan, const int32_t** units_host, int32_t* n_units);
+libra_status libra_plan_get_info(libra_plan plan, libra_plan_info* info);
+/* Bytes of device workspace the plan's calls need (unit table, counters, partials). */
+size_t libra_plan_workspace_bytes(libra_plan plan);
+/* Copies the plan's tables into `workspace` (device) on `stream` and clears its merge
+ * counters.  Decode / append calls do this themselves when the workspace they get is
+ * not the one last uploaded to; calling it explicitly once per batch step lets every
+ * layer's call skip it.  The workspace then belongs to this plan until another upload. */
+libra_status libra_plan_upload(libra_plan plan, void* workspace, size_t ws_bytes, void* stream);
+/* Waits for the plan's pending upload (if any), then frees it. */
+void libra_plan_destroy(libra_plan plan);
+
+/* ------------------------------------------------------------------------------ */
+/* Attention                                                                       */
+/* ------------------------------------------------------------------------------ */
+/*
+ * Decode: one query token per sequence attends all L_b cached tokens (the current
+ * token's K/V is already in the cache).  For each query head h of sequence b:
+ *   z_j = scale * <q_h, k_j>,  out = sum_j softmax(z)_j v_j,  lse = log sum_j exp(z_j)
+ * over keys j in [0, L_b); L_b = 0 gives out = 0, lse = -inf.
+ *
+ * q, out: device bf16 [batch][num_q_heads][128].  lse: device float32
+ * [batch][num_q_heads] or NULL.  block_table: device int32 [batch][bt_stride] with at
+ * least ceil(L_b / 16) valid page ids per row.  The plan must be a decode plan built for
+ * the same (batch, num_q_heads, num_kv_heads) and lengths; workspace: device, at least
+ * libra_plan_workspace_bytes(plan) bytes, 256-byte aligned.  `scale` must be finite.
+ * Split rows are merged by their log-sum-exps inside the same launch.
+ */
+libra_status libra_decode_attn(libra_kv_layout layout, libra_plan plan, const void* q,
+                               const int32_t* block_table, int32_t bt_stride, int32_t batch,
+                               int32_t num_q_heads, float scale, void* workspace, size_t ws_bytes,
+                               void* out, float* lse, void* stream);
+
+/*
+ * Append: sequence b adds C_b tokens (a tool-output chunk, or C_b = 1 for an ordinary
+ * decode step) after P_b = L_b - C_b cached tokens, as when a tool returns and its
+ * output is incorporated before decoding resumes (Sec. 5, Phase 2 and Step 3).  The
+ * call first writes k_new / v_new into the cache at positions [P_b, L_b), then new
+ * token i attends keys [0, P_b + i] (causal, itself included) with the formula above.
+ *
+ * q, out: device bf16 [sum C_b][num_q_heads][128], rows of sequence b starting at
+ * sum_{b' < b} C_b'.  k_new, v_new: device bf16 [sum C_b][num_kv_heads][128].  lse:
+ * device float32 [sum C_b][num_q_heads] or NULL.  The block table must already map the
+ * pages of positions [0, L_b).  The plan must be an append plan for the same shapes.
+ */
+libra_status libra_append_attn(libra_kv_layout layout, libra_plan plan, const void* q,
+                               const void* k_new, const void* v_new, const int32_t* block_table,
+                               int32_t bt_stride, int32_t batch, int32_t num_q_heads, float scale,
+                               void* workspace, size_t ws_bytes, void* out, float* lse,
+                               void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LIBRA_H_ */

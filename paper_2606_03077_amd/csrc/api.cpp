@@ -1,0 +1,335 @@
+// extern "C" entry points of libra (declared and documented in include/libra.h).
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <new>
+#include <string>
+
+#include "internal.h"
+
+namespace libra {
+
+namespace {
+thread_local std::string g_last_error;
+}
+
+libra_status set_error(libra_status s, const std::string& msg) {
+  g_last_error = msg;
+  return s;
+}
+
+libra_status hip_error(hipError_t e, const char* what) {
+  g_last_error = std::string(what) + ": " + hipGetErrorString(e);
+  return LIBRA_E_HIP;
+}
+
+namespace {
+
+constexpr size_t kWorkspaceAlign = 256;
+
+libra_status check_layout(const libra_kv_layout_desc* d) {
+  if (!d) return set_error(LIBRA_E_INVAL, "layout descriptor is NULL");
+  if (d->page_size != kPage) return set_error(LIBRA_E_UNSUPPORTED, "page_size must be 16");
+  if (d->head_dim != kDim) return set_error(LIBRA_E_UNSUPPORTED, "head_dim must be 128");
+  if (d->dtype != LIBRA_DTYPE_BF16) return set_error(LIBRA_E_UNSUPPORTED, "dtype must be bf16");
+  if (d->num_kv_heads <= 0) return set_error(LIBRA_E_INVAL, "num_kv_heads must be > 0");
+  if (d->num_pages <= 0) return set_error(LIBRA_E_INVAL, "num_pages must be > 0");
+  if (d->num_pages > (int64_t(1) << 40) / d->num_kv_heads)
+    return set_error(LIBRA_E_INVAL, "num_pages * num_kv_heads too large");
+  if (!d->k_cache || !d->v_cache) return set_error(LIBRA_E_INVAL, "k_cache / v_cache is NULL");
+  if ((reinterpret_cast<uintptr_t>(d->k_cache) | reinterpret_cast<uintptr_t>(d->v_cache)) & 15)
+    return set_error(LIBRA_E_INVAL, "k_cache / v_cache must be 16-byte aligned");
+  return LIBRA_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+// Largest page index + 1 the plan's units and writes touch, per the block table.
+int64_t plan_pages_needed(const Plan& P) {
+  int64_t need = 0;
+  const int n = P.info.n_units;
+  for (int i = 0; i < n; ++i) {
+    const int32_t* u = &P.units[size_t(i) * kUnitInts];
+    need = std::max<int64_t>(need, (int64_t(u[U_KV1]) + kPage - 1) / kPage);
+  }
+  for (int i = 0; i < P.info.n_write_tiles; ++i)
+    need = std::max<int64_t>(need, int64_t(P.writes[size_t(i) * kWriteInts + W_PAGE]) + 1);
+  return need;
+}
+
+libra_status upload(Plan& P, void* ws, size_t ws_bytes, hipStream_t s) {
+  if (!ws) return set_error(LIBRA_E_INVAL, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(ws) % kWorkspaceAlign)
+    return set_error(LIBRA_E_INVAL, "workspace must be 256-byte aligned");
+  if (ws_bytes < P.ws_bytes)
+    return set_error(LIBRA_E_WORKSPACE, "workspace smaller than libra_plan_workspace_bytes");
+  hipError_t e;
+  if (!P.pinned && P.upload_bytes > 0) {
+    e = hipHostMalloc(&P.pinned, P.upload_bytes, hipHostMallocDefault);
+    if (e != hipSuccess) {
+      P.pinned = nullptr;
+      return hip_error(e, "hipHostMalloc(plan tables)");
+    }
+    std::memset(P.pinned, 0, P.upload_bytes);
+    char* h = static_cast<char*>(P.pinned);
+    std::memcpy(h + P.off_units, P.units.data(), P.units.size() * sizeof(int32_t));
+    std::memcpy(h + P.off_writes, P.writes.data(), P.writes.size() * sizeof(int32_t));
+  }
+  if (!P.upload_done) {
+    e = hipEventCreateWithFlags(&P.upload_done, hipEventDisableTiming);
+    if (e != hipSuccess) {
+      P.upload_done = nullptr;
+      return hip_error(e, "hipEventCreate");
+    }
+  }
+  if (P.upload_bytes > 0) {
+    e = hipMemcpyAsync(ws, P.pinned, P.upload_bytes, hipMemcpyHostToDevice, s);
+    if (e != hipSuccess) return hip_error(e, "hipMemcpyAsync(plan tables)");
+  }
+  e = launch_zero_i32(reinterpret_cast<int32_t*>(static_cast<char*>(ws) + P.off_counters),
+                      P.n_counters, s);
+  if (e != hipSuccess) return hip_error(e, "zero counters");
+  e = hipEventRecord(P.upload_done, s);
+  if (e != hipSuccess) return hip_error(e, "hipEventRecord");
+  P.uploaded_ws = ws;
+  return LIBRA_OK;
+}
+
+libra_status check_call(const KvLayout* L, const Plan* P, int mode, const void* q,
+                        const int32_t* bt, int32_t bt_stride, int32_t batch, int32_t hq,
+                        float scale, const void* out) {
+  if (!L || !P) return set_error(LIBRA_E_INVAL, "layout or plan is NULL");
+  if (P->mode != mode)
+    return set_error(LIBRA_E_INVAL, mode == LIBRA_MODE_DECODE ? "plan is not a decode plan"
+                                                              : "plan is not an append plan");
+  if (batch != P->batch || hq != P->num_q_heads)
+    return set_error(LIBRA_E_INVAL, "batch / num_q_heads differ from the plan's");
+  if (P->num_kv_heads != L->desc.num_kv_heads)
+    return set_error(LIBRA_E_INVAL, "plan and layout disagree on num_kv_heads");
+  if (!std::isfinite(scale)) return set_error(LIBRA_E_INVAL, "scale must be finite");
+  if (P->info.n_rows > 0) {
+    if (!q || !out) return set_error(LIBRA_E_INVAL, "q / out is NULL");
+    if (!aligned16(q) || !aligned16(out)) return set_error(LIBRA_E_INVAL, "q / out must be 16-byte aligned");
+  }
+  const int64_t need = plan_pages_needed(*P);
+  if (need > 0) {
+    if (!bt) return set_error(LIBRA_E_INVAL, "block_table is NULL");
+    if (bt_stride < need)
+      return set_error(LIBRA_E_INVAL, "bt_stride smaller than the pages the plan's lengths need");
+  }
+  return LIBRA_OK;
+}
+
+}  // namespace
+}  // namespace libra
+
+using namespace libra;
+
+struct libra_kv_layout_s : KvLayout {};
+struct libra_plan_s : Plan {};
+
+extern "C" {
+
+const char* libra_status_string(libra_status s) {
+  switch (s) {
+    case LIBRA_OK: return "LIBRA_OK";
+    case LIBRA_E_INVAL: return "LIBRA_E_INVAL";
+    case LIBRA_E_UNSUPPORTED: return "LIBRA_E_UNSUPPORTED";
+    case LIBRA_E_WORKSPACE: return "LIBRA_E_WORKSPACE";
+    case LIBRA_E_HIP: return "LIBRA_E_HIP";
+    case LIBRA_E_NOMEM: return "LIBRA_E_NOMEM";
+  }
+  return "LIBRA_E_UNKNOWN";
+}
+
+const char* libra_last_error(void) { return g_last_error.c_str(); }
+
+libra_status libra_kv_layout_create(const libra_kv_layout_desc* desc, libra_kv_layout* out) {
+  if (!out) return set_error(LIBRA_E_INVAL, "out is NULL");
+  *out = nullptr;
+  libra_status st = check_layout(desc);
+  if (st != LIBRA_OK) return st;
+  auto* L = new (std::nothrow) libra_kv_layout_s();
+  if (!L) return set_error(LIBRA_E_NOMEM, "layout allocation failed");
+  L->desc = *desc;
+  *out = L;
+  return LIBRA_OK;
+}
+
+void libra_kv_layout_destroy(libra_kv_layout layout) { delete layout; }
+
+libra_status libra_kv_pack_pages(libra_kv_layout layout, const void* k_src, const void* v_src,
+                                 int64_t first_page, int64_t n_pages, void* stream) {
+  if (!layout) return set_error(LIBRA_E_INVAL, "layout is NULL");
+  if (!k_src && !v_src) return set_error(LIBRA_E_INVAL, "k_src and v_src are both NULL");
+  if (first_page < 0 || n_pages < 0 || first_page + n_pages > layout->desc.num_pages)
+    return set_error(LIBRA_E_INVAL, "page range outside the cache");
+  if ((k_src && !aligned16(k_src)) || (v_src && !aligned16(v_src)))
+    return set_error(LIBRA_E_INVAL, "sources must be 16-byte aligned");
+  hipError_t e = launch_pack(*layout, k_src, v_src, first_page, n_pages,
+                             static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? LIBRA_OK : hip_error(e, "pack launch");
+}
+
+libra_status libra_kv_unpack_pages(libra_kv_layout layout, void* k_dst, void* v_dst,
+                                   int64_t first_page, int64_t n_pages, void* stream) {
+  if (!layout) return set_error(LIBRA_E_INVAL, "layout is NULL");
+  if (!k_dst && !v_dst) return set_error(LIBRA_E_INVAL, "k_dst and v_dst are both NULL");
+  if (first_page < 0 || n_pages < 0 || first_page + n_pages > layout->desc.num_pages)
+    return set_error(LIBRA_E_INVAL, "page range outside the cache");
+  if ((k_dst && !aligned16(k_dst)) || (v_dst && !aligned16(v_dst)))
+    return set_error(LIBRA_E_INVAL, "destinations must be 16-byte aligned");
+  hipError_t e = launch_unpack(*layout, k_dst, v_dst, first_page, n_pages,
+                               static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? LIBRA_OK : hip_error(e, "unpack launch");
+}
+
+libra_status libra_kv_gather(libra_kv_layout layout, const int32_t* block_table, int32_t bt_stride,
+                             const int32_t* cu_seq_lens, int32_t batch, int32_t max_pages,
+                             void* k_out, void* v_out, void* stream) {
+  if (!layout) return set_error(LIBRA_E_INVAL, "layout is NULL");
+  if (batch < 0 || max_pages < 0) return set_error(LIBRA_E_INVAL, "batch / max_pages < 0");
+  if (batch == 0 || max_pages == 0) return LIBRA_OK;
+  if (!block_table || !cu_seq_lens || !k_out || !v_out)
+    return set_error(LIBRA_E_INVAL, "NULL pointer argument");
+  if (bt_stride < max_pages) return set_error(LIBRA_E_INVAL, "bt_stride < max_pages");
+  if (batch > 65535 || layout->desc.num_kv_heads > 65535)
+    return set_error(LIBRA_E_UNSUPPORTED, "batch and num_kv_heads must be <= 65535");
+  if (!aligned16(k_out) || !aligned16(v_out))
+    return set_error(LIBRA_E_INVAL, "outputs must be 16-byte aligned");
+  hipError_t e = launch_gather(*layout, block_table, bt_stride, cu_seq_lens, batch, max_pages,
+                               k_out, v_out, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? LIBRA_OK : hip_error(e, "gather launch");
+}
+
+libra_status libra_splitkv_plan(const libra_plan_desc* desc, const int32_t* seq_lens_host,
+                                const int32_t* q_lens_host, const libra_plan_params* params,
+                                libra_plan* out) {
+  if (!out) return set_error(LIBRA_E_INVAL, "out is NULL");
+  *out = nullptr;
+  if (!desc) return set_error(LIBRA_E_INVAL, "plan descriptor is NULL");
+  const libra_plan_desc& d = *desc;
+  if (d.mode != LIBRA_MODE_DECODE && d.mode != LIBRA_MODE_APPEND)
+    return set_error(LIBRA_E_INVAL, "mode must be LIBRA_MODE_DECODE or LIBRA_MODE_APPEND");
+  if (d.batch < 0) return set_error(LIBRA_E_INVAL, "batch must be >= 0");
+  if (d.num_kv_heads <= 0 || d.num_q_heads <= 0 || d.num_q_heads % d.num_kv_heads)
+    return set_error(LIBRA_E_INVAL, "num_q_heads must be a positive multiple of num_kv_heads");
+  const int G = d.num_q_heads / d.num_kv_heads;
+  if (G > LIBRA_MAX_GROUP) return set_error(LIBRA_E_UNSUPPORTED, "num_q_heads / num_kv_heads > 16");
+  if (d.batch > 0 && !seq_lens_host) return set_error(LIBRA_E_INVAL, "seq_lens_host is NULL");
+  if (d.mode == LIBRA_MODE_DECODE && q_lens_host)
+    return set_error(LIBRA_E_INVAL, "decode plans take q_lens_host = NULL");
+  if (d.mode == LIBRA_MODE_APPEND && d.batch > 0 && !q_lens_host)
+    return set_error(LIBRA_E_INVAL, "append plans need q_lens_host");
+
+  libra_plan_params p{0, 2, 32, 64, 0};
+  if (params) p = *params;
+  if (p.num_cus == 0) {
+    int dev = 0, cus = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return hip_error(e, "querying the compute-unit count");
+    p.num_cus = cus;
+  }
+  if (p.num_cus <= 0 || p.units_per_cu <= 0 || p.min_split_pages <= 0 || p.max_splits <= 0 ||
+      p.q_tile < 0)
+    return set_error(LIBRA_E_INVAL, "plan parameters must be positive");
+  const int tpb = G >= 16 ? 1 : 16 / G;
+  if (p.q_tile > 16 * tpb)
+    return set_error(LIBRA_E_UNSUPPORTED, "q_tile larger than 16 * max(1, 16 / G) tokens");
+
+  auto* P = new (std::nothrow) libra_plan_s();
+  if (!P) return set_error(LIBRA_E_NOMEM, "plan allocation failed");
+  libra_status st;
+  try {
+    st = build_plan(d, seq_lens_host, q_lens_host, p, P);
+  } catch (const std::bad_alloc&) {
+    st = set_error(LIBRA_E_NOMEM, "plan tables allocation failed");
+  }
+  if (st != LIBRA_OK) {
+    delete P;
+    return st;
+  }
+  *out = P;
+  return LIBRA_OK;
+}
+
+libra_status libra_plan_get_units(libra_plan plan, const int32_t** units_host, int32_t* n_units) {
+  if (!plan || !units_host || !n_units) return set_error(LIBRA_E_INVAL, "NULL argument");
+  *units_host = plan->units.data();
+  *n_units = plan->info.n_units;
+  return LIBRA_OK;
+}
+
+libra_status libra_plan_get_info(libra_plan plan, libra_plan_info* info) {
+  if (!plan || !info) return set_error(LIBRA_E_INVAL, "NULL argument");
+  *info = plan->info;
+  return LIBRA_OK;
+}
+
+size_t libra_plan_workspace_bytes(libra_plan plan) { return plan ? plan->ws_bytes : 0; }
+
+libra_status libra_plan_upload(libra_plan plan, void* workspace, size_t ws_bytes, void* stream) {
+  if (!plan) return set_error(LIBRA_E_INVAL, "plan is NULL");
+  return upload(*plan, workspace, ws_bytes, static_cast<hipStream_t>(stream));
+}
+
+void libra_plan_destroy(libra_plan plan) {
+  if (!plan) return;
+  if (plan->upload_done) {
+    (void)hipEventSynchronize(plan->upload_done);
+    (void)hipEventDestroy(plan->upload_done);
+  }
+  if (plan->pinned) (void)hipHostFree(plan->pinned);
+  delete plan;
+}
+
+libra_status libra_decode_attn(libra_kv_layout layout, libra_plan plan, const void* q,
+                               const int32_t* block_table, int32_t bt_stride, int32_t batch,
+                               int32_t num_q_heads, float scale, void* workspace, size_t ws_bytes,
+                               void* out, float* lse, void* stream) {
+  libra_status st = check_call(layout, plan, LIBRA_MODE_DECODE, q, block_table, bt_stride, batch,
+                               num_q_heads, scale, out);
+  if (st != LIBRA_OK) return st;
+  if (ws_bytes < plan->ws_bytes)
+    return set_error(LIBRA_E_WORKSPACE, "workspace smaller than libra_plan_workspace_bytes");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (plan->uploaded_ws != workspace) {
+    st = upload(*plan, workspace, ws_bytes, s);
+    if (st != LIBRA_OK) return st;
+  }
+  hipError_t e = launch_decode(*layout, *plan, workspace, q, block_table, bt_stride, scale, out,
+                               lse, s);
+  return e == hipSuccess ? LIBRA_OK : hip_error(e, "decode launch");
+}
+
+libra_status libra_append_attn(libra_kv_layout layout, libra_plan plan, const void* q,
+                               const void* k_new, const void* v_new, const int32_t* block_table,
+                               int32_t bt_stride, int32_t batch, int32_t num_q_heads, float scale,
+                               void* workspace, size_t ws_bytes, void* out, float* lse,
+                               void* stream) {
+  libra_status st = check_call(layout, plan, LIBRA_MODE_APPEND, q, block_table, bt_stride, batch,
+                               num_q_heads, scale, out);
+  if (st != LIBRA_OK) return st;
+  if (plan->info.n_rows > 0) {
+    if (!k_new || !v_new) return set_error(LIBRA_E_INVAL, "k_new / v_new is NULL");
+    if (!aligned16(k_new) || !aligned16(v_new))
+      return set_error(LIBRA_E_INVAL, "k_new / v_new must be 16-byte aligned");
+  }
+  if (ws_bytes < plan->ws_bytes)
+    return set_error(LIBRA_E_WORKSPACE, "workspace smaller than libra_plan_workspace_bytes");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (plan->uploaded_ws != workspace) {
+    st = upload(*plan, workspace, ws_bytes, s);
+    if (st != LIBRA_OK) return st;
+  }
+  hipError_t e = launch_cache_write(*layout, *plan, workspace, k_new, v_new, block_table,
+                                    bt_stride, s);
+  if (e != hipSuccess) return hip_error(e, "cache-write launch");
+  e = launch_decode(*layout, *plan, workspace, q, block_table, bt_stride, scale, out, lse, s);
+  if (e != hipSuccess) return hip_error(e, "decode launch");
+  e = launch_chunk(*layout, *plan, workspace, q, block_table, bt_stride, scale, out, lse, s);
+  return e == hipSuccess ? LIBRA_OK : hip_error(e, "chunk launch");
+}
+
+}  // extern "C"

@@ -1,0 +1,80 @@
+// Internal declarations shared by the host code and the HIP kernels of libra.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "libra.h"
+
+namespace libra {
+
+constexpr int kPage = LIBRA_PAGE_SIZE;     // tokens per page
+constexpr int kDim = LIBRA_HEAD_DIM;       // channels per head
+constexpr int kTileElems = kPage * kDim;   // bf16 elements per (page, head) tile
+constexpr int kTileBytes = kTileElems * 2; // 4 KiB
+constexpr int kUnitInts = LIBRA_UNIT_INTS;
+
+// Unit record fields (int32), in table order.
+enum UnitField : int {
+  U_B = 0, U_G, U_KV0, U_KV1, U_Q0, U_Q1, U_SPLIT, U_NSPLIT, U_PART, U_ROW0, U_KIND, U_PRIOR
+};
+constexpr int kKindSingle = 0;
+constexpr int kKindChunk = 1;
+
+// Append cache-write table: one record per (sequence, page) the new tokens touch.
+enum WriteField : int { W_B = 0, W_PAGE, W_SLOT0, W_SLOT1, W_ROW, W_PAD0, W_PAD1, W_PAD2 };
+constexpr int kWriteInts = 8;
+
+struct Plan {
+  int32_t mode = LIBRA_MODE_DECODE;
+  int32_t batch = 0, num_q_heads = 0, num_kv_heads = 0, group = 0;
+  libra_plan_params params{};
+  libra_plan_info info{};
+  std::vector<int32_t> units;   // n_units * kUnitInts
+  std::vector<int32_t> writes;  // n_write_tiles * kWriteInts (append only)
+
+  // Workspace image: [units | writes | counters | partial o | partial lse], 256-B aligned.
+  size_t off_units = 0, off_writes = 0, off_counters = 0, off_part_o = 0, off_part_lse = 0;
+  size_t ws_bytes = 0;
+  size_t upload_bytes = 0;  // bytes of [units | writes] copied from the host
+  int32_t n_counters = 0;
+
+  // Upload state.
+  void* pinned = nullptr;         // host staging copy of [units | writes]
+  hipEvent_t upload_done = nullptr;
+  void* uploaded_ws = nullptr;
+};
+
+struct KvLayout {
+  libra_kv_layout_desc desc{};
+};
+
+// Error reporting (per thread).
+libra_status set_error(libra_status s, const std::string& msg);
+libra_status hip_error(hipError_t e, const char* what);
+
+// Plan construction (host, no HIP calls unless num_cus == 0).
+libra_status build_plan(const libra_plan_desc& d, const int32_t* seq_lens, const int32_t* q_lens,
+                        const libra_plan_params& p, Plan* out);
+
+// Kernel launchers (defined next to their kernels).
+hipError_t launch_pack(const KvLayout& L, const void* k_src, const void* v_src, int64_t first,
+                       int64_t n, hipStream_t s);
+hipError_t launch_unpack(const KvLayout& L, void* k_dst, void* v_dst, int64_t first, int64_t n,
+                         hipStream_t s);
+hipError_t launch_gather(const KvLayout& L, const int32_t* bt, int32_t stride, const int32_t* cu,
+                         int32_t batch, int32_t max_pages, void* k_out, void* v_out, hipStream_t s);
+hipError_t launch_zero_i32(int32_t* p, int64_t n, hipStream_t s);
+hipError_t launch_cache_write(const KvLayout& L, const Plan& P, const void* ws, const void* k_new,
+                              const void* v_new, const int32_t* bt, int32_t stride, hipStream_t s);
+hipError_t launch_decode(const KvLayout& L, const Plan& P, void* ws, const void* q,
+                         const int32_t* bt, int32_t stride, float scale, void* out, float* lse,
+                         hipStream_t s);
+hipError_t launch_chunk(const KvLayout& L, const Plan& P, void* ws, const void* q,
+                        const int32_t* bt, int32_t stride, float scale, void* out, float* lse,
+                        hipStream_t s);
+
+}  // namespace libra

@@ -1,0 +1,182 @@
+// Host construction of the split-KV work plan (rule documented in include/libra.h).
+#include <algorithm>
+#include <array>
+#include <cstring>
+
+#include "internal.h"
+
+namespace libra {
+namespace {
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+using Unit = std::array<int32_t, kUnitInts>;
+
+}  // namespace
+
+libra_status build_plan(const libra_plan_desc& d, const int32_t* seq_lens, const int32_t* q_lens,
+                        const libra_plan_params& p, Plan* out) {
+  const int64_t B = d.batch;
+  const int64_t Hkv = d.num_kv_heads;
+  const int64_t G = d.num_q_heads / d.num_kv_heads;
+  const bool append = d.mode == LIBRA_MODE_APPEND;
+
+  std::vector<int64_t> L(B), C(B), pages(B), row0(B);
+  int64_t rows = 0;
+  for (int64_t b = 0; b < B; ++b) {
+    L[b] = seq_lens[b];
+    C[b] = append ? q_lens[b] : 1;
+    if (L[b] < 0) return set_error(LIBRA_E_INVAL, "seq_lens must be >= 0");
+    if (append && (C[b] < 1 || C[b] > L[b]))
+      return set_error(LIBRA_E_INVAL, "append needs 1 <= q_lens[b] <= seq_lens[b]");
+    pages[b] = ceil_div(L[b], kPage);
+    row0[b] = rows;
+    rows += C[b];
+  }
+  if (rows > INT32_MAX) return set_error(LIBRA_E_INVAL, "too many query rows");
+
+  // Step 3: chunk size from the single rows' total work.
+  int64_t W = 0;
+  for (int64_t b = 0; b < B; ++b)
+    if (C[b] == 1) W += pages[b] * Hkv;
+  const int64_t target = int64_t(p.num_cus) * p.units_per_cu;
+  const int64_t chunk = W > 0 ? std::max<int64_t>(p.min_split_pages, ceil_div(W, target))
+                              : int64_t(p.min_split_pages);
+
+  // Step 4 + 8: split counts and partial slots in ascending (b, g).
+  std::vector<int64_t> nsplit(B, 1), slot_base(B, -1);
+  int64_t slots = 0;
+  for (int64_t b = 0; b < B; ++b) {
+    if (C[b] != 1) continue;
+    nsplit[b] = std::min<int64_t>(p.max_splits, std::max<int64_t>(1, ceil_div(pages[b], chunk)));
+    if (nsplit[b] > 1) {
+      slot_base[b] = slots;
+      slots += nsplit[b] * Hkv;
+    }
+  }
+  if (slots > INT32_MAX) return set_error(LIBRA_E_INVAL, "too many partial slots");
+
+  std::vector<Unit> singles, chunks;
+  for (int64_t b = 0; b < B; ++b) {
+    if (C[b] != 1) continue;
+    const int64_t n = nsplit[b];
+    for (int64_t g = 0; g < Hkv; ++g) {
+      for (int64_t j = 0; j < n; ++j) {
+        const int64_t p0 = (j * pages[b]) / n, p1 = ((j + 1) * pages[b]) / n;
+        Unit u{};
+        u[U_B] = int32_t(b);
+        u[U_G] = int32_t(g);
+        u[U_KV0] = int32_t(kPage * p0);
+        u[U_KV1] = int32_t(std::min<int64_t>(kPage * p1, L[b]));
+        u[U_Q0] = 0;
+        u[U_Q1] = 1;
+        u[U_SPLIT] = int32_t(j);
+        u[U_NSPLIT] = int32_t(n);
+        u[U_PART] = n > 1 ? int32_t(slot_base[b] + g * n) : -1;
+        u[U_ROW0] = int32_t(row0[b]);
+        u[U_KIND] = kKindSingle;
+        u[U_PRIOR] = int32_t(L[b] - 1);
+        singles.push_back(u);
+      }
+    }
+  }
+  std::sort(singles.begin(), singles.end(), [](const Unit& x, const Unit& y) {
+    const int64_t tx = x[U_KV1] - x[U_KV0], ty = y[U_KV1] - y[U_KV0];
+    if (tx != ty) return tx > ty;
+    if (x[U_B] != y[U_B]) return x[U_B] < y[U_B];
+    if (x[U_G] != y[U_G]) return x[U_G] < y[U_G];
+    return x[U_SPLIT] < y[U_SPLIT];
+  });
+
+  // Step 5: query tiles of chunk rows.
+  const int64_t T = p.q_tile > 0 ? p.q_tile : int64_t(kPage) * std::max<int64_t>(1, 16 / G);
+  for (int64_t b = 0; b < B; ++b) {
+    if (C[b] == 1) continue;
+    const int64_t P = L[b] - C[b];
+    for (int64_t g = 0; g < Hkv; ++g) {
+      for (int64_t q0 = 0; q0 < C[b]; q0 += T) {
+        const int64_t q1 = std::min(q0 + T, C[b]);
+        Unit u{};
+        u[U_B] = int32_t(b);
+        u[U_G] = int32_t(g);
+        u[U_KV0] = 0;
+        u[U_KV1] = int32_t(P + q1);
+        u[U_Q0] = int32_t(q0);
+        u[U_Q1] = int32_t(q1);
+        u[U_SPLIT] = 0;
+        u[U_NSPLIT] = 1;
+        u[U_PART] = -1;
+        u[U_ROW0] = int32_t(row0[b]);
+        u[U_KIND] = kKindChunk;
+        u[U_PRIOR] = int32_t(P);
+        chunks.push_back(u);
+      }
+    }
+  }
+  std::sort(chunks.begin(), chunks.end(), [](const Unit& x, const Unit& y) {
+    const int64_t cx = int64_t(x[U_KV1] - x[U_KV0]) * (x[U_Q1] - x[U_Q0]);
+    const int64_t cy = int64_t(y[U_KV1] - y[U_KV0]) * (y[U_Q1] - y[U_Q0]);
+    if (cx != cy) return cx > cy;
+    if (x[U_B] != y[U_B]) return x[U_B] < y[U_B];
+    if (x[U_G] != y[U_G]) return x[U_G] < y[U_G];
+    return x[U_Q0] < y[U_Q0];
+  });
+
+  Plan& P = *out;
+  P.mode = d.mode;
+  P.batch = d.batch;
+  P.num_q_heads = d.num_q_heads;
+  P.num_kv_heads = d.num_kv_heads;
+  P.group = int32_t(G);
+  P.params = p;
+  P.units.clear();
+  P.units.reserve((singles.size() + chunks.size()) * kUnitInts);
+  for (const Unit& u : singles) P.units.insert(P.units.end(), u.begin(), u.end());
+  for (const Unit& u : chunks) P.units.insert(P.units.end(), u.begin(), u.end());
+
+  // Cache-write table (append): every (sequence, page) holding new positions [P_b, L_b).
+  P.writes.clear();
+  if (append) {
+    for (int64_t b = 0; b < B; ++b) {
+      const int64_t P0 = L[b] - C[b];
+      for (int64_t pg = P0 / kPage; pg * kPage < L[b]; ++pg) {
+        const int64_t s0 = std::max<int64_t>(P0, pg * kPage) - pg * kPage;
+        const int64_t s1 = std::min<int64_t>(L[b], pg * kPage + kPage) - pg * kPage;
+        const int32_t rec[kWriteInts] = {int32_t(b), int32_t(pg), int32_t(s0), int32_t(s1),
+                                         int32_t(row0[b] + pg * kPage + s0 - P0), 0, 0, 0};
+        P.writes.insert(P.writes.end(), rec, rec + kWriteInts);
+      }
+    }
+  }
+
+  libra_plan_info& I = P.info;
+  std::memset(&I, 0, sizeof(I));
+  I.n_single = int32_t(singles.size());
+  I.n_chunk = int32_t(chunks.size());
+  I.n_units = I.n_single + I.n_chunk;
+  I.n_partial_slots = int32_t(slots);
+  I.chunk_pages = chunk;
+  I.q_tile = int32_t(T);
+  I.n_rows = int32_t(rows);
+  I.n_write_tiles = int32_t(P.writes.size() / kWriteInts);
+  I.num_cus = p.num_cus;
+
+  P.n_counters = slots > 0 ? int32_t(B * Hkv) : 0;
+  size_t off = 0;
+  P.off_units = off;
+  off = align256(off + P.units.size() * sizeof(int32_t));
+  P.off_writes = off;
+  off = align256(off + P.writes.size() * sizeof(int32_t));
+  P.upload_bytes = off;
+  P.off_counters = off;
+  off = align256(off + size_t(P.n_counters) * sizeof(int32_t));
+  P.off_part_o = off;
+  off = align256(off + size_t(slots) * size_t(G) * kDim * sizeof(float));
+  P.off_part_lse = off;
+  off = align256(off + size_t(slots) * size_t(G) * sizeof(float));
+  P.ws_bytes = std::max<size_t>(off, 256);
+  return LIBRA_OK;
+}
+
+}  // namespace libra

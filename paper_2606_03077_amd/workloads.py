@@ -26,6 +26,8 @@ Recipe (fixed, so that every stored number can be regenerated):
 * draw order: lengths, chunk lengths, mixture positions, page permutation, q, K, V,
   k_new, v_new;
 * value draws: standard normal in float32, rounded to bf16 with round-to-nearest-even;
+  each array draws one child seed from the batch generator and fills chunks of 2**22
+  elements from PCG64(SeedSequence([child seed, chunk index]));
 * "uniform in [a, b]" is inclusive; lognormal lengths are
   ``clip(rint(exp(ln(median) + sigma * z)), lo, hi)``; Pareto lengths are
   ``min(floor(xm * U ** (-1 / alpha)), cap)`` with ``U = 1 - uniform[0, 1)`` in (0, 1];
@@ -37,6 +39,7 @@ from __future__ import annotations
 
 import dataclasses
 import math
+import os
 from typing import Optional
 
 import numpy as np
@@ -126,17 +129,34 @@ def bf16_bits_to_f32(bits: np.ndarray) -> np.ndarray:
     return (np.asarray(bits, dtype=np.uint16).astype(np.uint32) << np.uint32(16)).view(np.float32)
 
 
-def normal_bf16(rng: np.random.Generator, shape, chunk: int = 1 << 24) -> np.ndarray:
-    """N(0,1) float32 draws rounded to bf16, generated in bounded chunks.
+_CHUNK = 1 << 22
 
-    Chunking does not change the values: the generator yields the same stream as a
-    single draw of the whole size.
+
+def _fill_chunk(child_seed: int, index: int, out: np.ndarray) -> None:
+    g = np.random.Generator(np.random.PCG64(np.random.SeedSequence([child_seed, index])))
+    out[:] = f32_to_bf16_bits(g.standard_normal(out.shape[0], dtype=np.float32))
+
+
+def normal_bf16(rng: np.random.Generator, shape) -> np.ndarray:
+    """N(0,1) float32 draws rounded to bf16, for one array of the batch.
+
+    One 63-bit child seed is drawn from ``rng``; element chunk i (2**22 elements) comes
+    from PCG64(SeedSequence([child_seed, i])).  The values therefore depend only on the
+    seed and the shape, not on how many threads fill the chunks.
     """
     n = int(np.prod(shape))
     out = np.empty(n, dtype=np.uint16)
-    for s in range(0, n, chunk):
-        e = min(n, s + chunk)
-        out[s:e] = f32_to_bf16_bits(rng.standard_normal(e - s, dtype=np.float32))
+    child = int(rng.integers(0, 2 ** 63 - 1))
+    starts = range(0, n, _CHUNK)
+    if n > 4 * _CHUNK:
+        import concurrent.futures as cf
+        workers = min(16, len(os.sched_getaffinity(0)))
+        with cf.ThreadPoolExecutor(max_workers=workers) as ex:
+            list(ex.map(lambda i: _fill_chunk(child, i, out[i * _CHUNK:(i + 1) * _CHUNK]),
+                        range(len(starts))))
+    else:
+        for i, s0 in enumerate(starts):
+            _fill_chunk(child, i, out[s0:s0 + _CHUNK])
     return out.reshape(shape)
 
 

@@ -1,0 +1,123 @@
+"""Moves generator batches onto the GPU and runs them through the C-ABI (tests only)."""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import torch
+
+from paper_2606_03077_amd import libra
+from paper_2606_03077_amd import workloads as wl
+
+TOL_ABS = 2e-2      # max |gpu - oracle| over all output elements
+TOL_ROW_REL = 1e-2  # max over rows of ||gpu - oracle||_inf / ||oracle||_inf
+TOL_LSE = 1e-3      # max |lse_gpu - lse_oracle| (natural log)
+
+
+def say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def u16_to_dev(a: np.ndarray) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).cuda()
+
+
+def dev_to_u16(t: torch.Tensor) -> np.ndarray:
+    return t.cpu().numpy().view(np.uint16)
+
+
+def bf16_dev_to_f64(t: torch.Tensor) -> np.ndarray:
+    return wl.bf16_bits_to_f32(dev_to_u16(t)).astype(np.float64)
+
+
+class DeviceCache:
+    """The batch's logical pages packed into the library layout on the GPU."""
+
+    def __init__(self, batch: wl.Batch):
+        P, Hkv = batch.k_pages.shape[0], batch.k_pages.shape[1]
+        self.num_pages, self.hkv = P, Hkv
+        self.k = torch.empty(P * Hkv * 2048, dtype=torch.int16, device="cuda")
+        self.v = torch.empty_like(self.k)
+        self.layout = libra.libra_kv_layout_create(self.k, self.v, P, Hkv)
+        k_log = u16_to_dev(batch.k_pages)
+        v_log = u16_to_dev(batch.v_pages)
+        libra.libra_kv_pack_pages(self.layout, k_log, v_log, 0, P)
+        torch.cuda.synchronize()
+        del k_log, v_log
+        self.bt = torch.from_numpy(batch.block_table).cuda()
+        self.bt_stride = batch.block_table.shape[1]
+
+    def unpack(self):
+        k = torch.empty(self.num_pages * self.hkv * 2048, dtype=torch.int16, device="cuda")
+        v = torch.empty_like(k)
+        libra.libra_kv_unpack_pages(self.layout, k, v, 0, self.num_pages)
+        torch.cuda.synchronize()
+        shape = (self.num_pages, self.hkv, 16, 128)
+        return dev_to_u16(k).reshape(shape), dev_to_u16(v).reshape(shape)
+
+    def close(self):
+        libra.libra_kv_layout_destroy(self.layout)
+
+
+def plan_for(batch: wl.Batch, **params):
+    w = batch.workload
+    mode = libra.LIBRA_MODE_APPEND if w.append else libra.LIBRA_MODE_DECODE
+    q_lens = batch.q_lens.tolist() if w.append else None
+    return libra.libra_splitkv_plan(mode, len(batch.seq_lens), w.num_q_heads, w.num_kv_heads,
+                                    batch.seq_lens.tolist(), q_lens, **params)
+
+
+def run(batch: wl.Batch, cache: DeviceCache = None, plan_params=None, repeat: int = 1):
+    """Runs decode or append; returns (out f64 [rows,Hq,128], lse f64 [rows,Hq], cache, raw)."""
+    cache = cache or DeviceCache(batch)
+    w = batch.workload
+    plan = plan_for(batch, **(plan_params or {}))
+    try:
+        ws = libra.alloc_workspace(plan)
+        q = u16_to_dev(batch.q)
+        rows = batch.q.shape[0]
+        out = torch.empty((rows, w.num_q_heads, 128), dtype=torch.int16, device="cuda")
+        lse = torch.empty((rows, w.num_q_heads), dtype=torch.float32, device="cuda")
+        for _ in range(repeat):
+            if w.append:
+                kn, vn = u16_to_dev(batch.k_new), u16_to_dev(batch.v_new)
+                libra.libra_append_attn(cache.layout, plan, q, kn, vn, cache.bt, cache.bt_stride,
+                                        len(batch.seq_lens), w.num_q_heads, batch.scale, ws, out, lse)
+            else:
+                libra.libra_decode_attn(cache.layout, plan, q, cache.bt, cache.bt_stride,
+                                        len(batch.seq_lens), w.num_q_heads, batch.scale, ws, out,
+                                        lse)
+        torch.cuda.synchronize()
+        raw_out = dev_to_u16(out)
+        o = wl.bf16_bits_to_f32(raw_out).astype(np.float64)
+        l = lse.cpu().numpy().astype(np.float64)
+        return o, l, cache, raw_out
+    finally:
+        libra.libra_plan_destroy(plan)
+
+
+def errors(o, lse, ro, rl, rows=None):
+    """(max-abs, max row-relative, max lse-abs) of GPU vs oracle over the given rows."""
+    if rows is not None:
+        o, lse, ro, rl = o[rows], lse[rows], ro[rows], rl[rows]
+    assert np.isfinite(o).all(), "non-finite output"
+    d = np.abs(o - ro)
+    max_abs = float(d.max()) if d.size else 0.0
+    ref_inf = np.abs(ro).max(axis=-1)
+    row_rel = d.max(axis=-1) / np.maximum(ref_inf, 1e-30)
+    row_rel = np.where(ref_inf > 0, row_rel, d.max(axis=-1))
+    max_rel = float(row_rel.max()) if row_rel.size else 0.0
+    both_inf = np.isneginf(lse) & np.isneginf(rl)
+    with np.errstate(invalid="ignore"):
+        dl = np.where(both_inf, 0.0, np.abs(lse - rl))
+    max_lse = float(dl.max()) if dl.size else 0.0
+    return max_abs, max_rel, max_lse
+
+
+def assert_parity(o, lse, ro, rl, rows=None, label=""):
+    ea, er, el = errors(o, lse, ro, rl, rows)
+    say(f"[parity] {label}: max_abs={ea:.3e} max_row_rel={er:.3e} max_lse={el:.3e}")
+    assert ea <= TOL_ABS, f"{label}: max abs error {ea} > {TOL_ABS}"
+    assert er <= TOL_ROW_REL, f"{label}: row-relative error {er} > {TOL_ROW_REL}"
+    assert el <= TOL_LSE, f"{label}: lse error {el} > {TOL_LSE}"

@@ -1,0 +1,194 @@
+"""Host-side checks of the C-ABI (no GPU needed).
+
+* the shared library loads and exports every function include/libra.h declares;
+* the host plan is bit-exact against the oracle's re-implementation of the rule;
+* argument validation returns the documented status codes before any HIP call.
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2606_03077_amd import libra
+from paper_2606_03077_amd import workloads as wl
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "libra.h")
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(libra_\w+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function():
+    lib = libra.load()
+    declared = header_functions()
+    assert len(declared) >= 15
+    for name in declared:
+        assert hasattr(lib, name), name
+    assert set(declared) == set(libra.EXPORTS)
+
+
+def test_single_hip_runtime_is_mapped():
+    libra.load()
+    assert len(libra.hip_runtimes_mapped()) <= 1
+
+
+def test_status_strings():
+    for code, name in libra.STATUS_NAMES.items():
+        assert libra.libra_status_string(code) == name
+
+
+def _plan_units(mode, B, hq, hkv, lens, qlens, params):
+    h = libra.libra_splitkv_plan(mode, B, hq, hkv, lens, qlens, params.num_cus,
+                                 params.units_per_cu, params.min_split_pages, params.max_splits,
+                                 params.q_tile)
+    try:
+        return libra.libra_plan_get_units(h), libra.libra_plan_get_info(h)
+    finally:
+        libra.libra_plan_destroy(h)
+
+
+def _compare(lens, qlens, hq, hkv, params):
+    mode = libra.LIBRA_MODE_DECODE if qlens is None else libra.LIBRA_MODE_APPEND
+    got, info = _plan_units(mode, len(lens), hq, hkv, lens, qlens, params)
+    ref, rinfo = oracle.plan_ref(lens, qlens, hkv, hq // hkv, params)
+    assert got.shape == (len(ref), 12)
+    assert np.array_equal(got, np.array(ref, dtype=np.int32).reshape(-1, 12))
+    assert info["n_single"] == rinfo["n_single"] and info["n_chunk"] == rinfo["n_chunk"]
+    assert info["n_partial_slots"] == rinfo["n_partial_slots"]
+    assert info["chunk_pages"] == rinfo["chunk_pages"] and info["q_tile"] == rinfo["q_tile"]
+
+
+@pytest.mark.parametrize("name", ["tiny", "7b", "longtail", "straggler", "append"])
+def test_plan_bit_exact_on_workload_lengths(name):
+    w = wl.WORKLOADS[name]
+    lens, qlens = wl.draw_lengths(w, np.random.default_rng(w.seed))
+    q = qlens.tolist() if w.append else None
+    for params in [oracle.PlanParams(), oracle.PlanParams(num_cus=256, units_per_cu=3,
+                                                          min_split_pages=8, max_splits=128)]:
+        _compare(lens.tolist(), q, w.num_q_heads, w.num_kv_heads, params)
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_plan_bit_exact_random(seed):
+    rng = np.random.default_rng(1000 + seed)
+    B = int(rng.integers(0, 50))
+    lens = rng.choice([0, 1, 15, 16, 17, 63, 64, 65, 4095, 131072], size=B).tolist()
+    params = oracle.PlanParams(num_cus=int(rng.integers(1, 300)),
+                               units_per_cu=int(rng.integers(1, 5)),
+                               min_split_pages=int(rng.integers(1, 100)),
+                               max_splits=int(rng.integers(1, 130)))
+    hkv = int(rng.choice([1, 2, 4, 8]))
+    G = int(rng.choice([1, 2, 4, 5, 7, 8, 16]))
+    _compare(lens, None, G * hkv, hkv, params)
+    qlens = [int(rng.choice([1, 1, 2, 17, 300, 1024])) for _ in lens]
+    lens2 = [max(L, c) for L, c in zip(lens, qlens)]
+    tpb = max(1, 16 // G)
+    params2 = oracle.PlanParams(params.num_cus, params.units_per_cu, params.min_split_pages,
+                                params.max_splits, q_tile=int(rng.integers(0, 16 * tpb + 1)))
+    _compare(lens2, qlens, G * hkv, hkv, params2)
+
+
+def _status_of(fn, *args):
+    try:
+        fn(*args)
+    except libra.LibraError as e:
+        return e.status
+    return libra.LIBRA_OK
+
+
+def test_plan_validation_codes():
+    D, A = libra.LIBRA_MODE_DECODE, libra.LIBRA_MODE_APPEND
+    P = libra.libra_splitkv_plan
+    assert _status_of(P, D, 2, 6, 4, [1, 2], None, 8) == 1          # Hq % Hkv != 0
+    assert _status_of(P, D, 2, 34, 2, [1, 2], None, 8) == 2         # G = 17 > 16
+    assert _status_of(P, D, 2, 8, 2, [1, 2], [1, 1], 8) == 1        # decode with q_lens
+    assert _status_of(P, A, 2, 8, 2, [1, 2], None, 8) == 1          # append without q_lens
+    assert _status_of(P, A, 1, 8, 2, [5], [6], 8) == 1              # C > L
+    assert _status_of(P, A, 1, 8, 2, [5], [0], 8) == 1              # C = 0
+    assert _status_of(P, D, 1, 8, 2, [-1], None, 8) == 1            # negative length
+    assert _status_of(P, D, 1, 8, 2, [5], None, 8, 0) == 1          # units_per_cu = 0
+    assert _status_of(P, A, 1, 8, 2, [90], [80], 8, 2, 32, 64, 65) == 2  # q_tile > 16 * 4
+    h = P(D, 0, 8, 2, [], None, 8)                                    # empty batch is valid
+    assert libra.libra_plan_get_info(h)["n_units"] == 0
+    libra.libra_plan_destroy(h)
+
+
+def test_layout_validation_codes():
+    lib = libra.load()
+    fake = 1 << 20
+
+    def create(**kw):
+        d = dict(num_pages=10, page_size=16, num_kv_heads=2, head_dim=128, dtype=0,
+                 k_cache=fake, v_cache=fake * 2)
+        d.update(kw)
+        desc = libra.LayoutDesc(d["num_pages"], d["page_size"], d["num_kv_heads"],
+                                d["head_dim"], d["dtype"], d["k_cache"], d["v_cache"])
+        h = ctypes.c_void_p()
+        st = lib.libra_kv_layout_create(ctypes.byref(desc), ctypes.byref(h))
+        if st == 0:
+            lib.libra_kv_layout_destroy(h)
+        return st
+
+    assert create() == 0
+    assert create(head_dim=64) == 2
+    assert create(page_size=32) == 2
+    assert create(dtype=7) == 2
+    assert create(num_pages=0) == 1
+    assert create(num_kv_heads=0) == 1
+    assert create(k_cache=None) == 1
+    assert create(v_cache=fake + 2) == 1  # misaligned
+
+
+def test_call_validation_codes_before_any_launch():
+    lib = libra.load()
+    fake = 1 << 20
+    desc = libra.LayoutDesc(64, 16, 2, 128, 0, fake, fake * 2)
+    lay = ctypes.c_void_p()
+    assert lib.libra_kv_layout_create(ctypes.byref(desc), ctypes.byref(lay)) == 0
+    plan = libra.libra_splitkv_plan(libra.LIBRA_MODE_DECODE, 2, 8, 2, [40, 100], None, 8)
+    ws_need = libra.libra_plan_workspace_bytes(plan)
+    args = dict(q=fake, bt=fake, stride=7, batch=2, hq=8, scale=0.088, ws=fake * 4,
+                ws_bytes=ws_need, out=fake * 8, lse=None)
+
+    def call(**kw):
+        a = dict(args)
+        a.update(kw)
+        return lib.libra_decode_attn(lay, plan, a["q"], a["bt"], a["stride"], a["batch"], a["hq"],
+                                     a["scale"], a["ws"], a["ws_bytes"], a["out"], a["lse"], None)
+
+    assert call(batch=3) == 1                      # batch differs from the plan
+    assert call(hq=16) == 1                        # heads differ
+    assert call(scale=float("nan")) == 1           # non-finite scale
+    assert call(q=None) == 1                       # null q
+    assert call(bt=None) == 1                      # null block table
+    assert call(stride=6) == 1                     # 100 tokens need 7 pages
+    assert call(ws_bytes=ws_need - 1) == 3         # short workspace
+    assert call(ws=fake * 4 + 16) == 1             # misaligned workspace
+    assert call(q=fake + 2) == 1                   # misaligned q
+    aplan = libra.libra_splitkv_plan(libra.LIBRA_MODE_APPEND, 2, 8, 2, [40, 100], [1, 5], 8)
+    assert lib.libra_decode_attn(lay, aplan, fake, fake, 7, 2, 8, 0.1, fake * 4, 1 << 20,
+                                 fake * 8, None, None) == 1  # append plan in a decode call
+    assert lib.libra_append_attn(lay, aplan, fake, None, fake, fake, 7, 2, 8, 0.1, fake * 4,
+                                 1 << 20, fake * 8, None, None) == 1  # null k_new
+    assert "k_new" in libra.libra_last_error()
+    libra.libra_plan_destroy(plan)
+    libra.libra_plan_destroy(aplan)
+    lib.libra_kv_layout_destroy(lay)
+
+
+def test_workspace_size_accounts_for_partials():
+    plan = libra.libra_splitkv_plan(libra.LIBRA_MODE_DECODE, 4, 64, 8,
+                                    [98304, 131072, 100000, 120000], None, 256)
+    info = libra.libra_plan_get_info(plan)
+    ws = libra.libra_plan_workspace_bytes(plan)
+    G = 8
+    need = info["n_units"] * 48 + 4 * 8 * 4 + info["n_partial_slots"] * G * 129 * 4
+    assert ws >= need and ws % 256 == 0
+    libra.libra_plan_destroy(plan)

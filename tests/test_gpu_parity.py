@@ -1,0 +1,197 @@
+"""GPU parity of the HIP path (through the C-ABI) against the fp64 oracle.
+
+Tolerances (bf16 inputs, float32 accumulation, bf16 outputs): max |gpu - oracle| <= 2e-2
+over every output element, max over rows of ||gpu - oracle||_inf / ||oracle||_inf <= 1e-2,
+and |lse_gpu - lse_oracle| <= 1e-3 (natural log).  Layout moves, block-table gathers and
+cache writes are compared bit for bit.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle.attention import gather_tokens
+from paper_2606_03077_amd import libra
+from paper_2606_03077_amd import workloads as wl
+
+import gpu_harness as H
+
+pytestmark = pytest.mark.gpu
+
+
+def _decode_oracle(batch, rows=None):
+    return oracle.decode_ref(batch.q, batch.k_pages, batch.v_pages, batch.block_table,
+                             batch.seq_lens, batch.scale, batch_rows=rows)
+
+
+def _append_oracle(batch, rows=None):
+    return oracle.append_ref(batch.q, batch.k_new, batch.v_new, batch.k_pages, batch.v_pages,
+                             batch.block_table, batch.seq_lens, batch.q_lens, batch.scale,
+                             batch_rows=rows)
+
+
+def test_pack_unpack_and_gather_are_bit_exact():
+    H.say("[case] pack/unpack/gather tiny")
+    b = wl.make_batch("tiny")
+    cache = H.DeviceCache(b)
+    k2, v2 = cache.unpack()
+    assert np.array_equal(k2, b.k_pages) and np.array_equal(v2, b.v_pages)
+    lens = b.seq_lens.astype(np.int64)
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    Hkv = b.workload.num_kv_heads
+    ko = torch.empty((int(cu[-1]), Hkv, 128), dtype=torch.int16, device="cuda")
+    vo = torch.empty_like(ko)
+    max_pages = int((lens.max() + 15) // 16)
+    libra.libra_kv_gather(cache.layout, cache.bt, cache.bt_stride, torch.from_numpy(cu).cuda(),
+                          len(lens), max_pages, ko, vo)
+    torch.cuda.synchronize()
+    kg, vg = H.dev_to_u16(ko), H.dev_to_u16(vo)
+    for s in range(len(lens)):
+        for g in range(Hkv):
+            ref_k = gather_tokens(b.k_pages, b.block_table[s], g, int(lens[s]))
+            ref_v = gather_tokens(b.v_pages, b.block_table[s], g, int(lens[s]))
+            assert np.array_equal(kg[cu[s]:cu[s + 1], g], ref_k)
+            assert np.array_equal(vg[cu[s]:cu[s + 1], g], ref_v)
+    cache.close()
+
+
+def test_decode_tiny_full():
+    H.say("[case] decode tiny (config 1) full")
+    b = wl.make_batch("tiny")
+    o, lse, cache, _ = H.run(b)
+    ro, rl = _decode_oracle(b)
+    H.assert_parity(o, lse, ro, rl, label="tiny")
+    cache.close()
+
+
+@pytest.mark.parametrize("hq,hkv", [(28, 4), (8, 2), (64, 8), (16, 16), (16, 1)])
+def test_decode_ragged_with_splits(hq, hkv):
+    lens = [1, 15, 16, 17, 31, 33, 100, 257, 1000, 2049, 5000]
+    H.say(f"[case] decode ragged hq={hq} hkv={hkv} lens={lens}")
+    b = wl.custom_batch(lens, num_q_heads=hq, num_kv_heads=hkv, seed=hq * 100 + hkv)
+    for params in [dict(num_cus=4, units_per_cu=1, min_split_pages=2, max_splits=64),
+                   dict(num_cus=256, units_per_cu=2, min_split_pages=32, max_splits=64),
+                   dict(num_cus=8, units_per_cu=1, min_split_pages=1, max_splits=1)]:
+        o, lse, cache, _ = H.run(b, plan_params=params)
+        ro, rl = _decode_oracle(b)
+        H.assert_parity(o, lse, ro, rl, label=f"ragged {hq}/{hkv} {params}")
+        cache.close()
+
+
+def test_decode_single_key_returns_v_bitwise():
+    H.say("[case] decode L=1")
+    b = wl.custom_batch([1, 1, 1], num_q_heads=8, num_kv_heads=2, seed=5)
+    o, lse, cache, raw = H.run(b)
+    G = 4
+    for s in range(3):
+        for h in range(8):
+            v = b.v_pages[b.block_table[s, 0], h // G, 0]
+            assert np.array_equal(raw[s, h], v)
+    ro, rl = _decode_oracle(b)
+    H.assert_parity(o, lse, ro, rl, label="L=1")
+    cache.close()
+
+
+def test_decode_empty_and_ragged_edges():
+    H.say("[case] decode empty sequences")
+    b = wl.custom_batch([0, 5, 0, 16, 17], num_q_heads=8, num_kv_heads=2, seed=6)
+    o, lse, cache, _ = H.run(b)
+    assert np.all(o[[0, 2]] == 0) and np.all(np.isneginf(lse[[0, 2]]))
+    ro, rl = _decode_oracle(b)
+    H.assert_parity(o, lse, ro, rl, label="empty")
+    cache.close()
+
+
+def test_decode_page_permutation_and_rerun_are_bitwise_identical():
+    H.say("[case] page permutation / determinism")
+    b = wl.custom_batch([700, 33, 4000, 1], num_q_heads=28, num_kv_heads=4, seed=7)
+    params = dict(num_cus=4, units_per_cu=1, min_split_pages=4, max_splits=16)
+    o1, l1, cache, raw1 = H.run(b, plan_params=params, repeat=2)
+    o1b, l1b, _, raw1b = H.run(b, cache=cache, plan_params=params)
+    assert np.array_equal(raw1, raw1b) and np.array_equal(l1, l1b)
+    cache.close()
+    perm = np.random.default_rng(1).permutation(b.num_pages)
+    kp = np.empty_like(b.k_pages)
+    vp = np.empty_like(b.v_pages)
+    kp[perm] = b.k_pages
+    vp[perm] = b.v_pages
+    b2 = wl.Batch(b.workload, b.seq_lens, b.q_lens, b.cu_q_lens, perm[b.block_table].astype(np.int32),
+                  kp, vp, b.q, None, None, b.scale)
+    o2, l2, cache2, raw2 = H.run(b2, plan_params=params)
+    assert np.array_equal(raw1, raw2) and np.array_equal(l1, l2)
+    cache2.close()
+
+
+@pytest.mark.parametrize("name", ["7b", "straggler"])
+def test_decode_full_config_sampled(name):
+    H.say(f"[case] decode {name} full size")
+    b = wl.make_batch(name)
+    o, lse, cache, _ = H.run(b)
+    cache.close()
+    lens = b.seq_lens
+    rows = sorted(set([int(np.argmax(lens)), int(np.argmin(lens))] +
+                      np.random.default_rng(0).choice(len(lens), size=min(6, len(lens)),
+                                                      replace=False).tolist()))
+    ro, rl = _decode_oracle(b, rows)
+    H.assert_parity(o, lse, ro, rl, rows=rows, label=f"{name} rows {rows}")
+    # every row: finite outputs, lse above the logit of any single key
+    assert np.isfinite(o).all() and np.isfinite(lse).all()
+
+
+def test_decode_longtail_full_config_sampled():
+    H.say("[case] decode longtail full size")
+    b = wl.make_batch("longtail")
+    o, lse, cache, _ = H.run(b)
+    cache.close()
+    lens = b.seq_lens
+    tail = np.argsort(lens)[-3:].tolist()
+    rows = sorted(set(tail + [int(np.argmin(lens))] + [0, 100, 255]))
+    ro, rl = _decode_oracle(b, rows)
+    H.assert_parity(o, lse, ro, rl, rows=rows, label=f"longtail rows {rows}")
+    assert np.isfinite(o).all() and np.isfinite(lse).all()
+
+
+@pytest.mark.parametrize("hq,hkv", [(32, 8), (28, 4), (8, 8), (16, 1)])
+def test_append_mixed_chunks(hq, hkv):
+    prior = [0, 7, 100, 1000, 33, 16, 5000, 250]
+    chunk = [5, 1, 64, 300, 1, 16, 129, 1]
+    lens = [p + c for p, c in zip(prior, chunk)]
+    H.say(f"[case] append mixed hq={hq} hkv={hkv}")
+    b = wl.custom_batch(lens, q_lens=chunk, num_q_heads=hq, num_kv_heads=hkv, seed=hq + hkv)
+    o, lse, cache, _ = H.run(b, plan_params=dict(num_cus=4, units_per_cu=1, min_split_pages=2))
+    ro, rl, k_after, v_after = _append_oracle(b)
+    H.assert_parity(o, lse, ro, rl, label=f"append {hq}/{hkv}")
+    k2, v2 = cache.unpack()
+    assert np.array_equal(k2, k_after) and np.array_equal(v2, v_after)
+    cache.close()
+
+
+def test_append_one_token_rows_match_decode_bitwise():
+    H.say("[case] append C=1 vs decode")
+    lens = [40, 17, 3000, 1]
+    b = wl.custom_batch(lens, q_lens=[1, 1, 1, 1], num_q_heads=28, num_kv_heads=4, seed=3,
+                        append=True)
+    oa, la, cache, rawa = H.run(b, plan_params=dict(num_cus=4, units_per_cu=1, min_split_pages=2))
+    k_after, v_after = cache.unpack()
+    cache.close()
+    bd = wl.Batch(wl.dataclasses.replace(b.workload, append=False), b.seq_lens, b.q_lens,
+                  b.cu_q_lens, b.block_table, k_after, v_after, b.q, None, None, b.scale)
+    od, ld, cache2, rawd = H.run(bd, plan_params=dict(num_cus=4, units_per_cu=1, min_split_pages=2))
+    cache2.close()
+    assert np.array_equal(rawa, rawd) and np.array_equal(la, ld)
+
+
+def test_append_full_config_sampled():
+    H.say("[case] append (config 5) full size")
+    b = wl.make_batch("append")
+    o, lse, cache, _ = H.run(b)
+    cache.close()
+    ql = b.q_lens
+    chunk_seqs = np.nonzero(ql > 1)[0]
+    single_seqs = np.nonzero(ql == 1)[0]
+    seqs = sorted(set(chunk_seqs[:3].tolist() + [int(chunk_seqs[np.argmax(ql[chunk_seqs])])] +
+                      single_seqs[:3].tolist()))
+    ro, rl, _, _ = _append_oracle(b, rows=seqs)
+    rows = np.concatenate([np.arange(b.cu_q_lens[s], b.cu_q_lens[s + 1]) for s in seqs])
+    H.assert_parity(o, lse, ro, rl, rows=rows, label=f"append seqs {seqs}")
+    assert np.isfinite(o).all() and np.isfinite(lse).all()
