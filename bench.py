@@ -2,8 +2,8 @@
 
     python bench.py [--gpus 1] [--steps 50] [--warmup 5] [--workload 7b]
 
-One step = one decode-attention call (split-KV decode kernel with the fused
-log-sum-exp merge) over the whole synthetic batch, inputs resident in HBM.  Before each
+One step = one decode-attention call (the split-KV decode kernel, then the log-sum-exp
+merge of split rows) over the whole synthetic batch, inputs resident in HBM.  Before each
 timed step an untimed 1 GiB fill evicts L2 and the 256 MB MALL, so every step reads its
 KV from HBM.  Each step is bracketed by HIP events on the stream the kernel runs on.
 The host-side split plan is built once per batch step and shared by all layers of a
@@ -132,6 +132,9 @@ def main():
     ap.add_argument("--workload", default="7b",
                     choices=["tiny", "7b", "longtail", "straggler", "append"])
     ap.add_argument("--flush-mib", type=int, default=1024)
+    ap.add_argument("--units-per-cu", type=int, default=4)
+    ap.add_argument("--min-split-pages", type=int, default=16)
+    ap.add_argument("--max-splits", type=int, default=64)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     args = ap.parse_args()
@@ -179,15 +182,17 @@ def main():
 
     mode = libra.LIBRA_MODE_APPEND if w.append else libra.LIBRA_MODE_DECODE
     ql = batch.q_lens.tolist() if w.append else None
+    plan_kw = dict(units_per_cu=args.units_per_cu, min_split_pages=args.min_split_pages,
+                   max_splits=args.max_splits)
     plan_times = []
     for _ in range(5):
         t = time.perf_counter()
         plan = libra.libra_splitkv_plan(mode, len(batch.seq_lens), w.num_q_heads, Hkv,
-                                        batch.seq_lens.tolist(), ql)
+                                        batch.seq_lens.tolist(), ql, **plan_kw)
         plan_times.append((time.perf_counter() - t) * 1e3)
         libra.libra_plan_destroy(plan)
     plan = libra.libra_splitkv_plan(mode, len(batch.seq_lens), w.num_q_heads, Hkv,
-                                    batch.seq_lens.tolist(), ql)
+                                    batch.seq_lens.tolist(), ql, **plan_kw)
     info = libra.libra_plan_get_info(plan)
     ws = libra.alloc_workspace(plan)
     stream = torch.cuda.current_stream()
@@ -253,8 +258,8 @@ def main():
         "step_ms_p10_p50_p90": [round(p10, 5), round(p50, 5), round(p90, 5)],
         "timed_wall_s": round(wall, 4),
         "plan_ms": round(float(np.median(plan_times)), 4),
-        "plan": {k: info[k] for k in ("n_units", "n_single", "n_chunk", "n_partial_slots",
-                                      "chunk_pages", "num_cus")},
+        "plan": dict({k: info[k] for k in ("n_units", "n_single", "n_chunk", "n_partial_slots",
+                                           "chunk_pages", "num_cus")}, **plan_kw),
         "roofline": {
             "bound": "hbm",
             "achieved": round(achieved_gbs, 2),

@@ -155,8 +155,8 @@ libra_status libra_kv_gather(libra_kv_layout layout, const int32_t* block_table,
  */
 typedef struct libra_plan_params {
   int32_t num_cus;          /* compute units; 0 = query the current device */
-  int32_t units_per_cu;     /* default 2 */
-  int32_t min_split_pages;  /* default 32 */
+  int32_t units_per_cu;     /* default 4 */
+  int32_t min_split_pages;  /* default 16 */
   int32_t max_splits;       /* default 64 */
   int32_t q_tile;           /* chunk query tile in tokens; 0 = 16 * max(1, 16 / G) */
 } libra_plan_params;
@@ -178,6 +178,7 @@ typedef struct libra_plan_info {
   int32_t n_rows;           /* query rows (sum C_b) */
   int32_t n_write_tiles;    /* (sequence, page) pairs an append writes */
   int32_t num_cus;          /* CUs the plan was cut for */
+  int32_t n_merge_groups;   /* (sequence, KV head) pairs whose splits are merged */
 } libra_plan_info;
 
 /* Builds the plan from host lengths.  seq_lens_host: int32 [batch], L_b >= 0 (>= C_b
@@ -189,12 +190,14 @@ libra_status libra_splitkv_plan(const libra_plan_desc* desc, const int32_t* seq_
 /* Host view of the unit table (valid until libra_plan_destroy). */
 libra_status libra_plan_get_units(libra_plan plan, const int32_t** units_host, int32_t* n_units);
 libra_status libra_plan_get_info(libra_plan plan, libra_plan_info* info);
-/* Bytes of device workspace the plan's calls need (unit table, counters, partials). */
+/* Bytes of device workspace the plan's calls need (unit, write and merge tables and the
+ * float32 partial results of split rows). */
 size_t libra_plan_workspace_bytes(libra_plan plan);
-/* Copies the plan's tables into `workspace` (device) on `stream` and clears its merge
- * counters.  Decode / append calls do this themselves when the workspace they get is
- * not the one last uploaded to; calling it explicitly once per batch step lets every
- * layer's call skip it.  The workspace then belongs to this plan until another upload. */
+/* Copies the plan's tables into `workspace` (device) on `stream`.  Decode / append calls
+ * do this themselves when the workspace they get is not the one last uploaded to;
+ * calling it explicitly once per batch step lets every layer's call skip it.  The
+ * workspace then belongs to this plan until another upload; calls that share a
+ * workspace must be ordered on one stream. */
 libra_status libra_plan_upload(libra_plan plan, void* workspace, size_t ws_bytes, void* stream);
 /* Waits for the plan's pending upload (if any), then frees it. */
 void libra_plan_destroy(libra_plan plan);
@@ -213,7 +216,8 @@ void libra_plan_destroy(libra_plan plan);
  * least ceil(L_b / 16) valid page ids per row.  The plan must be a decode plan built for
  * the same (batch, num_q_heads, num_kv_heads) and lengths; workspace: device, at least
  * libra_plan_workspace_bytes(plan) bytes, 256-byte aligned.  `scale` must be finite.
- * Split rows are merged by their log-sum-exps inside the same launch.
+ * Split rows write float32 partials; a second launch on the same stream merges them by
+ * their log-sum-exps.
  */
 libra_status libra_decode_attn(libra_kv_layout layout, libra_plan plan, const void* q,
                                const int32_t* block_table, int32_t bt_stride, int32_t batch,

@@ -51,8 +51,8 @@ PAGE = 16
 @dataclasses.dataclass(frozen=True)
 class PlanParams:
     num_cus: int = 256
-    units_per_cu: int = 2
-    min_split_pages: int = 32
+    units_per_cu: int = 4
+    min_split_pages: int = 16
     max_splits: int = 64
     q_tile: int = 0
 

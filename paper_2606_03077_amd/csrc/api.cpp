@@ -74,6 +74,7 @@ libra_status upload(Plan& P, void* ws, size_t ws_bytes, hipStream_t s) {
     char* h = static_cast<char*>(P.pinned);
     std::memcpy(h + P.off_units, P.units.data(), P.units.size() * sizeof(int32_t));
     std::memcpy(h + P.off_writes, P.writes.data(), P.writes.size() * sizeof(int32_t));
+    std::memcpy(h + P.off_merges, P.merges.data(), P.merges.size() * sizeof(int32_t));
   }
   if (!P.upload_done) {
     e = hipEventCreateWithFlags(&P.upload_done, hipEventDisableTiming);
@@ -222,7 +223,7 @@ libra_status libra_splitkv_plan(const libra_plan_desc* desc, const int32_t* seq_
   if (d.mode == LIBRA_MODE_APPEND && d.batch > 0 && !q_lens_host)
     return set_error(LIBRA_E_INVAL, "append plans need q_lens_host");
 
-  libra_plan_params p{0, 2, 32, 64, 0};
+  libra_plan_params p{0, 4, 16, 64, 0};
   if (params) p = *params;
   if (p.num_cus == 0) {
     int dev = 0, cus = 0;
@@ -300,7 +301,9 @@ libra_status libra_decode_attn(libra_kv_layout layout, libra_plan plan, const vo
   }
   hipError_t e = launch_decode(*layout, *plan, workspace, q, block_table, bt_stride, scale, out,
                                lse, s);
-  return e == hipSuccess ? LIBRA_OK : hip_error(e, "decode launch");
+  if (e != hipSuccess) return hip_error(e, "decode launch");
+  e = launch_merge(*plan, workspace, out, lse, s);
+  return e == hipSuccess ? LIBRA_OK : hip_error(e, "merge launch");
 }
 
 libra_status libra_append_attn(libra_kv_layout layout, libra_plan plan, const void* q,
@@ -329,7 +332,9 @@ libra_status libra_append_attn(libra_kv_layout layout, libra_plan plan, const vo
   e = launch_decode(*layout, *plan, workspace, q, block_table, bt_stride, scale, out, lse, s);
   if (e != hipSuccess) return hip_error(e, "decode launch");
   e = launch_chunk(*layout, *plan, workspace, q, block_table, bt_stride, scale, out, lse, s);
-  return e == hipSuccess ? LIBRA_OK : hip_error(e, "chunk launch");
+  if (e != hipSuccess) return hip_error(e, "chunk launch");
+  e = launch_merge(*plan, workspace, out, lse, s);
+  return e == hipSuccess ? LIBRA_OK : hip_error(e, "merge launch");
 }
 
 }  // extern "C"

@@ -14,9 +14,10 @@
 // by occupancy (several workgroups per CU) rather than deep per-wave buffering.  Softmax runs online
 // in base 2 with the scale folded in; column maxima use two cross-lane shuffles.
 // The 4 waves' (max, sum, accumulator) are merged through LDS.  A unit that covers the
-// whole row writes bf16 O and the float32 LSE; a split writes a float32 partial and
-// the last split of its row to finish (atomic counter) merges all partials by their
-// log-sum-exps and resets the counter for the next call.
+// whole row writes bf16 O and the float32 LSE; a split writes a float32 partial, and
+// merge_kernel, launched next on the same stream, combines the partials of each split
+// row by their log-sum-exps (the launch boundary orders the two without device-wide
+// cache flushes inside either kernel).
 #include <cmath>
 
 #include "internal.h"
@@ -29,6 +30,16 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
+#ifndef LIBRA_DECODE_DEPTH
+#define LIBRA_DECODE_DEPTH 2
+#endif
+#ifndef LIBRA_FUSED_MERGE
+#define LIBRA_FUSED_MERGE 0
+#endif
+#ifndef LIBRA_DECODE_WAVES_PER_EU
+#define LIBRA_DECODE_WAVES_PER_EU 3
+#endif
+constexpr int kDepth = LIBRA_DECODE_DEPTH;  // pages of K/V held in registers per wave
 constexpr int kRedStride = 132;  // padded row of the LDS accumulator exchange
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
@@ -40,11 +51,20 @@ struct PageRegs {
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 x) { return __builtin_bit_cast(bf16x8, x); }
 
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// K/V bytes are read exactly once per call: non-temporal loads keep them from
+// displacing reusable lines and measurably raise the sustained random-tile read rate.
+__device__ __forceinline__ uint4 stream_load(const uint4* p) {
+  const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
 __device__ __forceinline__ void load_page(PageRegs& r, const uint4* kt, const uint4* vt, int lane) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i) r.k[i] = kt[i * 64 + lane];
+  for (int i = 0; i < 4; ++i) r.k[i] = stream_load(kt + i * 64 + lane);
 #pragma unroll
-  for (int i = 0; i < 4; ++i) r.v[i] = vt[i * 64 + lane];
+  for (int i = 0; i < 4; ++i) r.v[i] = stream_load(vt + i * 64 + lane);
 }
 
 // Zero V of slots >= valid (slot = 4 * quad + r): keeps NaN/garbage of unused slots
@@ -129,9 +149,9 @@ struct DecodeArgs {
   const uint16_t* q;
   uint16_t* out;
   float* lse;
-  int32_t* counters;
   float* part_o;
   float* part_lse;
+  int32_t* counters;
   int64_t bt_stride;
   int hkv;
   int hq;
@@ -139,11 +159,13 @@ struct DecodeArgs {
   float sl2;  // scale * log2(e)
 };
 
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3, 8))) void decode_kernel(DecodeArgs A) {
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(LIBRA_DECODE_WAVES_PER_EU, 8))) void decode_kernel(DecodeArgs A) {
   __shared__ float red_m[kWaves][16];
   __shared__ float red_l[kWaves][16];
   __shared__ __align__(16) float red_o[kWaves][16][kRedStride];
-  __shared__ int last_flag;
+#if LIBRA_FUSED_MERGE
+  __shared__ int red_flag;
+#endif
 
   const int32_t* u = A.units + size_t(blockIdx.x) * kUnitInts;
   const int b = u[U_B], g = u[U_G], kv0 = u[U_KV0], kv1 = u[U_KV1];
@@ -204,16 +226,21 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3, 8))
       process_page(r, valid, quad, qop, A.sl2, sm, acc);
     };
 
-    PageRegs r0, r1;
-    issue(0, r0);
-    int k = 0;
-    for (; k + 2 <= nw; k += 2) {
-      issue(k + 1, r1);
-      consume(r0, k);
-      if (k + 2 < nw) issue(k + 2, r0);
-      consume(r1, k + 1);
+    // Ring of kDepth pages: page k + kDepth is issued into the registers page k has
+    // just been consumed from, so kDepth - 1 pages stay in flight during the math.
+    PageRegs ring[kDepth];
+#pragma unroll
+    for (int j = 0; j < kDepth; ++j)
+      if (j < nw) issue(j, ring[j]);
+    for (int k = 0; k < nw; k += kDepth) {
+#pragma unroll
+      for (int j = 0; j < kDepth; ++j) {
+        if (k + j < nw) {
+          consume(ring[j], k + j);
+          if (k + j + kDepth < nw) issue(k + j + kDepth, ring[j]);
+        }
+      }
     }
-    if (k < nw) consume(r0, k);
   }
 
   // Column sum over the 4 key quads.
@@ -272,44 +299,48 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3, 8))
     return;
   }
 
-  // Split: publish the partial, then the last split of this (b, g) merges.
+  // Split: store this range's normalised float32 partial and its base-2 log-sum-exp.
   const size_t slot = size_t(part) + split;
+#if LIBRA_FUSED_MERGE
+  // The last split of a (sequence, KV head) to finish merges all of them.  Partials,
+  // counters and the merge's reads are agent-scope atomics, which the memory model keeps
+  // coherent across XCDs without whole-L2 write-backs or invalidations; s_waitcnt makes
+  // this workgroup's partial stores complete before its counter increment.
   if (hcol < G) {
     float* po = A.part_o + (slot * G + hcol) * kDim + c8;
-    *reinterpret_cast<f32x4*>(po) = f32x4{o[0], o[1], o[2], o[3]};
-    *reinterpret_cast<f32x4*>(po + 4) = f32x4{o[4], o[5], o[6], o[7]};
-    if ((tid & 15) == 0) A.part_lse[slot * G + hcol] = lse2;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) __hip_atomic_store(po + i, o[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if ((tid & 15) == 0)
+      __hip_atomic_store(A.part_lse + slot * G + hcol, lse2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
-  __threadfence();
+  __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
+  int32_t* ctr = A.counters + size_t(b) * A.hkv + g;
   if (tid == 0) {
-    int32_t* ctr = A.counters + size_t(b) * A.hkv + g;
-    const int prev = __hip_atomic_fetch_add(ctr, 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-    last_flag = prev == nsplit - 1;
+    const int prev = __hip_atomic_fetch_add(ctr, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    red_flag = prev == nsplit - 1;
   }
   __syncthreads();
-  if (!last_flag) return;
-  __threadfence();
+  if (!red_flag) return;
   if (hcol < G) {
     const size_t s0 = size_t(part);
     float Mg = -INFINITY;
-    for (int j = 0; j < nsplit; ++j) Mg = fmaxf(Mg, A.part_lse[(s0 + j) * G + hcol]);
+    for (int j = 0; j < nsplit; ++j)
+      Mg = fmaxf(Mg, __hip_atomic_load(A.part_lse + (s0 + j) * G + hcol, __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT));
     float acc8[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     float wsum = 0.f;
     if (Mg != -INFINITY) {
       for (int j = 0; j < nsplit; ++j) {
-        const float lj = A.part_lse[(s0 + j) * G + hcol];
+        const float lj = __hip_atomic_load(A.part_lse + (s0 + j) * G + hcol, __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_AGENT);
         if (lj == -INFINITY) continue;
         const float wj = __builtin_amdgcn_exp2f(lj - Mg);
         wsum += wj;
         const float* po = A.part_o + ((s0 + j) * G + hcol) * kDim + c8;
-        const f32x4 x0 = *reinterpret_cast<const f32x4*>(po);
-        const f32x4 x1 = *reinterpret_cast<const f32x4*>(po + 4);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          acc8[i] += wj * x0[i];
-          acc8[4 + i] += wj * x1[i];
-        }
+        for (int i = 0; i < 8; ++i)
+          acc8[i] += wj * __hip_atomic_load(po + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
     }
     const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
@@ -322,7 +353,88 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3, 8))
     if (A.lse && (tid & 15) == 0)
       A.lse[size_t(row) * A.hq + head] = wsum > 0.f ? (Mg + log2f(wsum)) * kLn2 : -INFINITY;
   }
-  if (tid == 0) A.counters[size_t(b) * A.hkv + g] = 0;
+  if (tid == 0) __hip_atomic_store(ctr, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+#else
+  // merge_kernel combines the splits after this launch.
+  if (hcol < G) {
+    float* po = A.part_o + (slot * G + hcol) * kDim + c8;
+    *reinterpret_cast<f32x4*>(po) = f32x4{o[0], o[1], o[2], o[3]};
+    *reinterpret_cast<f32x4*>(po + 4) = f32x4{o[4], o[5], o[6], o[7]};
+    if ((tid & 15) == 0) A.part_lse[slot * G + hcol] = lse2;
+  }
+#endif
+}
+
+struct MergeArgs {
+  const int32_t* merges;
+  const float* part_o;
+  const float* part_lse;
+  uint16_t* out;
+  float* lse;
+  int hq;
+  int group;
+};
+
+// One 256-thread block per split (sequence, KV head): thread t finishes channels
+// 8 * (t % 16) .. + 7 of query head t / 16 of the group.  With M = max_j lse_j (base 2):
+// lse = M + log2(sum_j 2^(lse_j - M)), o = sum_j 2^(lse_j - lse) o_j; empty splits
+// (lse_j = -inf) add nothing.  Splits are read 8 at a time (all loads of a batch in
+// flight together) and folded in with a running maximum.
+__global__ __launch_bounds__(kThreads) void merge_kernel(MergeArgs A) {
+  constexpr int kBatch = 8;
+  const int32_t* m = A.merges + size_t(blockIdx.x) * kMergeInts;
+  const int g = m[M_G], n = m[M_N], part = m[M_PART], row = m[M_ROW];
+  const int G = A.group;
+  const int tid = threadIdx.x;
+  const int hcol = tid >> 4, c8 = (tid & 15) * 8;
+  if (hcol >= G) return;
+  float M = -INFINITY, wsum = 0.f;
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  for (int j0 = 0; j0 < n; j0 += kBatch) {
+    float lj[kBatch];
+    f32x4 x0[kBatch], x1[kBatch];
+#pragma unroll
+    for (int jj = 0; jj < kBatch; ++jj) {
+      lj[jj] = -INFINITY;
+      x0[jj] = x1[jj] = f32x4{0.f, 0.f, 0.f, 0.f};
+      if (j0 + jj < n) {
+        const size_t slot = size_t(part + j0 + jj) * G + hcol;
+        lj[jj] = A.part_lse[slot];
+        const float* po = A.part_o + slot * kDim + c8;
+        x0[jj] = *reinterpret_cast<const f32x4*>(po);
+        x1[jj] = *reinterpret_cast<const f32x4*>(po + 4);
+      }
+    }
+    float Mc = M;
+#pragma unroll
+    for (int jj = 0; jj < kBatch; ++jj) Mc = fmaxf(Mc, lj[jj]);
+    if (Mc == -INFINITY) continue;
+    const float r = __builtin_amdgcn_exp2f(M - Mc);  // 0 while M = -inf
+    wsum *= r;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[i] *= r;
+#pragma unroll
+    for (int jj = 0; jj < kBatch; ++jj) {
+      const float w = __builtin_amdgcn_exp2f(lj[jj] - Mc);  // 0 for empty or absent splits
+      wsum += w;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        acc[i] += w * x0[jj][i];
+        acc[4 + i] += w * x1[jj][i];
+      }
+    }
+    M = Mc;
+  }
+  const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
+  uint4 ov;
+  ov.x = pack_bf16x2(acc[0] * inv, acc[1] * inv);
+  ov.y = pack_bf16x2(acc[2] * inv, acc[3] * inv);
+  ov.z = pack_bf16x2(acc[4] * inv, acc[5] * inv);
+  ov.w = pack_bf16x2(acc[6] * inv, acc[7] * inv);
+  const size_t head = size_t(g) * G + hcol;
+  *reinterpret_cast<uint4*>(A.out + (size_t(row) * A.hq + head) * kDim + c8) = ov;
+  if (A.lse && (tid & 15) == 0)
+    A.lse[size_t(row) * A.hq + head] = wsum > 0.f ? (M + log2f(wsum)) * kLn2 : -INFINITY;
 }
 
 }  // namespace
@@ -341,15 +453,35 @@ hipError_t launch_decode(const KvLayout& L, const Plan& P, void* ws, const void*
   A.q = static_cast<const uint16_t*>(q);
   A.out = static_cast<uint16_t*>(out);
   A.lse = lse;
-  A.counters = reinterpret_cast<int32_t*>(w + P.off_counters);
   A.part_o = reinterpret_cast<float*>(w + P.off_part_o);
   A.part_lse = reinterpret_cast<float*>(w + P.off_part_lse);
+  A.counters = reinterpret_cast<int32_t*>(w + P.off_counters);
   A.bt_stride = stride;
   A.hkv = P.num_kv_heads;
   A.hq = P.num_q_heads;
   A.group = P.group;
   A.sl2 = scale * kLog2e;
   hipLaunchKernelGGL(decode_kernel, dim3(unsigned(n)), dim3(kThreads), 0, s, A);
+  return hipGetLastError();
+}
+
+}  // namespace libra
+
+namespace libra {
+
+hipError_t launch_merge(const Plan& P, void* ws, void* out, float* lse, hipStream_t s) {
+  const int n = P.info.n_merge_groups;
+  if (n == 0 || LIBRA_FUSED_MERGE) return hipSuccess;
+  char* w = static_cast<char*>(ws);
+  MergeArgs A;
+  A.merges = reinterpret_cast<const int32_t*>(w + P.off_merges);
+  A.part_o = reinterpret_cast<const float*>(w + P.off_part_o);
+  A.part_lse = reinterpret_cast<const float*>(w + P.off_part_lse);
+  A.out = static_cast<uint16_t*>(out);
+  A.lse = lse;
+  A.hq = P.num_q_heads;
+  A.group = P.group;
+  hipLaunchKernelGGL(merge_kernel, dim3(unsigned(n)), dim3(kThreads), 0, s, A);
   return hipGetLastError();
 }
 

@@ -28,6 +28,10 @@ constexpr int kKindChunk = 1;
 enum WriteField : int { W_B = 0, W_PAGE, W_SLOT0, W_SLOT1, W_ROW, W_PAD0, W_PAD1, W_PAD2 };
 constexpr int kWriteInts = 8;
 
+// Split-merge table: one record per (sequence, KV head) whose KV range was split.
+enum MergeField : int { M_B = 0, M_G, M_N, M_PART, M_ROW, M_PAD0, M_PAD1, M_PAD2 };
+constexpr int kMergeInts = 8;
+
 struct Plan {
   int32_t mode = LIBRA_MODE_DECODE;
   int32_t batch = 0, num_q_heads = 0, num_kv_heads = 0, group = 0;
@@ -35,15 +39,19 @@ struct Plan {
   libra_plan_info info{};
   std::vector<int32_t> units;   // n_units * kUnitInts
   std::vector<int32_t> writes;  // n_write_tiles * kWriteInts (append only)
+  std::vector<int32_t> merges;  // n_merge_groups * kMergeInts
 
-  // Workspace image: [units | writes | counters | partial o | partial lse], 256-B aligned.
-  size_t off_units = 0, off_writes = 0, off_counters = 0, off_part_o = 0, off_part_lse = 0;
-  size_t ws_bytes = 0;
-  size_t upload_bytes = 0;  // bytes of [units | writes] copied from the host
+  // Workspace image: [units | writes | merges | counters | partial o | partial lse],
+  // 256-B aligned.  Counters (one per sequence x KV head when any row is split) start at
+  // zero after an upload and are returned to zero by the split merge.
+  size_t off_units = 0, off_writes = 0, off_merges = 0, off_counters = 0, off_part_o = 0,
+         off_part_lse = 0;
   int32_t n_counters = 0;
+  size_t ws_bytes = 0;
+  size_t upload_bytes = 0;  // bytes of [units | writes | merges] copied from the host
 
   // Upload state.
-  void* pinned = nullptr;         // host staging copy of [units | writes]
+  void* pinned = nullptr;         // host staging copy of [units | writes | merges]
   hipEvent_t upload_done = nullptr;
   void* uploaded_ws = nullptr;
 };
@@ -67,12 +75,13 @@ hipError_t launch_unpack(const KvLayout& L, void* k_dst, void* v_dst, int64_t fi
                          hipStream_t s);
 hipError_t launch_gather(const KvLayout& L, const int32_t* bt, int32_t stride, const int32_t* cu,
                          int32_t batch, int32_t max_pages, void* k_out, void* v_out, hipStream_t s);
-hipError_t launch_zero_i32(int32_t* p, int64_t n, hipStream_t s);
 hipError_t launch_cache_write(const KvLayout& L, const Plan& P, const void* ws, const void* k_new,
                               const void* v_new, const int32_t* bt, int32_t stride, hipStream_t s);
 hipError_t launch_decode(const KvLayout& L, const Plan& P, void* ws, const void* q,
                          const int32_t* bt, int32_t stride, float scale, void* out, float* lse,
                          hipStream_t s);
+hipError_t launch_zero_i32(int32_t* p, int64_t n, hipStream_t s);
+hipError_t launch_merge(const Plan& P, void* ws, void* out, float* lse, hipStream_t s);
 hipError_t launch_chunk(const KvLayout& L, const Plan& P, void* ws, const void* q,
                         const int32_t* bt, int32_t stride, float scale, void* out, float* lse,
                         hipStream_t s);

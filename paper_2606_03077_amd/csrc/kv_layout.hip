@@ -136,12 +136,20 @@ __global__ __launch_bounds__(kThreads) void cache_write_kernel(
   *reinterpret_cast<uint4*>(v_cache + base + t * 8) = *reinterpret_cast<const uint4*>(vt + t * 8);
 }
 
+// Clears the split-merge counters (a kernel rather than a memset, so that the upload
+// can be captured in a HIP graph).
 __global__ void zero_i32_kernel(int32_t* p, int64_t n) {
   const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
   if (i < n) p[i] = 0;
 }
 
 }  // namespace
+
+hipError_t launch_zero_i32(int32_t* p, int64_t n, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(zero_i32_kernel, dim3(unsigned((n + 255) / 256)), dim3(256), 0, s, p, n);
+  return hipGetLastError();
+}
 
 hipError_t launch_pack(const KvLayout& L, const void* k_src, const void* v_src, int64_t first,
                        int64_t n, hipStream_t s) {
@@ -176,12 +184,6 @@ hipError_t launch_gather(const KvLayout& L, const int32_t* bt, int32_t stride, c
                      dim3(kThreads), 0, s, static_cast<const uint16_t*>(L.desc.k_cache),
                      static_cast<const uint16_t*>(L.desc.v_cache), bt, stride, cu, hkv,
                      static_cast<uint16_t*>(k_out), static_cast<uint16_t*>(v_out));
-  return hipGetLastError();
-}
-
-hipError_t launch_zero_i32(int32_t* p, int64_t n, hipStream_t s) {
-  if (n == 0) return hipSuccess;
-  hipLaunchKernelGGL(zero_i32_kernel, dim3(unsigned((n + 255) / 256)), dim3(256), 0, s, p, n);
   return hipGetLastError();
 }
 

@@ -150,6 +150,18 @@ libra_status build_plan(const libra_plan_desc& d, const int32_t* seq_lens, const
     }
   }
 
+  // Split-merge table: every single row with n_b > 1, per KV head, ascending (b, g).
+  P.merges.clear();
+  for (int64_t b = 0; b < B; ++b) {
+    if (C[b] != 1 || nsplit[b] <= 1) continue;
+    for (int64_t g = 0; g < Hkv; ++g) {
+      const int32_t rec[kMergeInts] = {int32_t(b), int32_t(g), int32_t(nsplit[b]),
+                                       int32_t(slot_base[b] + g * nsplit[b]), int32_t(row0[b]),
+                                       0, 0, 0};
+      P.merges.insert(P.merges.end(), rec, rec + kMergeInts);
+    }
+  }
+
   libra_plan_info& I = P.info;
   std::memset(&I, 0, sizeof(I));
   I.n_single = int32_t(singles.size());
@@ -161,14 +173,17 @@ libra_status build_plan(const libra_plan_desc& d, const int32_t* seq_lens, const
   I.n_rows = int32_t(rows);
   I.n_write_tiles = int32_t(P.writes.size() / kWriteInts);
   I.num_cus = p.num_cus;
+  I.n_merge_groups = int32_t(P.merges.size() / kMergeInts);
 
-  P.n_counters = slots > 0 ? int32_t(B * Hkv) : 0;
   size_t off = 0;
   P.off_units = off;
   off = align256(off + P.units.size() * sizeof(int32_t));
   P.off_writes = off;
   off = align256(off + P.writes.size() * sizeof(int32_t));
+  P.off_merges = off;
+  off = align256(off + P.merges.size() * sizeof(int32_t));
   P.upload_bytes = off;
+  P.n_counters = slots > 0 ? int32_t(B * Hkv) : 0;
   P.off_counters = off;
   off = align256(off + size_t(P.n_counters) * sizeof(int32_t));
   P.off_part_o = off;

@@ -195,3 +195,32 @@ def test_append_full_config_sampled():
     rows = np.concatenate([np.arange(b.cu_q_lens[s], b.cu_q_lens[s + 1]) for s in seqs])
     H.assert_parity(o, lse, ro, rl, rows=rows, label=f"append seqs {seqs}")
     assert np.isfinite(o).all() and np.isfinite(lse).all()
+
+
+def test_split_merge_sees_fresh_partials_when_workspace_is_reused():
+    """Same lengths, different values, one plan and one workspace: every call must merge
+    its own partials (stale ones from the previous call would go unnoticed with equal
+    inputs), and the merge counters must return to zero after each call."""
+    lens = [3000, 17, 5000, 129, 2048]
+    H.say(f"[case] workspace reuse lens={lens}")
+    batches = [wl.custom_batch(lens, num_q_heads=28, num_kv_heads=4, seed=s) for s in (21, 22, 23)]
+    w = batches[0].workload
+    plan = libra.libra_splitkv_plan(libra.LIBRA_MODE_DECODE, len(lens), 28, 4, lens, None,
+                                    num_cus=64, units_per_cu=1, min_split_pages=2)
+    assert libra.libra_plan_get_info(plan)["n_partial_slots"] > 0
+    ws = libra.alloc_workspace(plan)
+    caches = [H.DeviceCache(b) for b in batches]
+    qs = [H.u16_to_dev(b.q) for b in batches]
+    refs = [_decode_oracle(b) for b in batches]
+    out = torch.empty((len(lens), 28, 128), dtype=torch.int16, device="cuda")
+    lse = torch.empty((len(lens), 28), dtype=torch.float32, device="cuda")
+    for i in [0, 1, 2, 1, 0, 2, 2, 0]:
+        libra.libra_decode_attn(caches[i].layout, plan, qs[i], caches[i].bt, caches[i].bt_stride,
+                                len(lens), 28, batches[i].scale, ws, out, lse)
+        torch.cuda.synchronize()
+        o = H.bf16_dev_to_f64(out)
+        H.assert_parity(o, lse.cpu().numpy().astype(np.float64), refs[i][0], refs[i][1],
+                        label=f"reuse call batch {i}")
+    for c in caches:
+        c.close()
+    libra.libra_plan_destroy(plan)
