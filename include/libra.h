@@ -242,6 +242,37 @@ libra_status libra_append_attn(libra_kv_layout layout, libra_plan plan, const vo
                                void* workspace, size_t ws_bytes, void* out, float* lse,
                                void* stream);
 
+/* ------------------------------------------------------------------------------ */
+/* Per-kernel timing                                                               */
+/* ------------------------------------------------------------------------------ */
+/*
+ * When enabled (process-wide), every kernel the library enqueues is bracketed by a pair
+ * of HIP events on the caller's stream.  libra_profile_collect waits for all recorded
+ * events, adds up elapsed milliseconds per kernel kind into *out and clears the record.
+ * Used to measure each kernel's own duration inside a multi-kernel call (and to fit
+ * per-operator latency models from measured timings).  Off by default; enabling it
+ * adds two event records per launch.  Not for use under HIP graph capture.
+ */
+enum {
+  LIBRA_KERNEL_PACK = 0,
+  LIBRA_KERNEL_UNPACK = 1,
+  LIBRA_KERNEL_GATHER = 2,
+  LIBRA_KERNEL_CACHE_WRITE = 3,
+  LIBRA_KERNEL_DECODE = 4,
+  LIBRA_KERNEL_MERGE = 5,
+  LIBRA_KERNEL_CHUNK = 6,
+  LIBRA_KERNEL_UPLOAD = 7,
+  LIBRA_KERNEL_KINDS = 8
+};
+
+typedef struct libra_kernel_times {
+  double ms[LIBRA_KERNEL_KINDS];       /* summed elapsed time per kernel kind */
+  int64_t launches[LIBRA_KERNEL_KINDS];
+} libra_kernel_times;
+
+libra_status libra_profile_enable(int enable);
+libra_status libra_profile_collect(libra_kernel_times* out);
+
 #ifdef __cplusplus
 }
 #endif

@@ -2,8 +2,10 @@
 #include <algorithm>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
+#include <vector>
 
 #include "internal.h"
 
@@ -26,6 +28,60 @@ libra_status hip_error(hipError_t e, const char* what) {
 namespace {
 
 constexpr size_t kWorkspaceAlign = 256;
+
+// Per-kernel timing: event pairs recorded around launches while enabled.
+struct Profiler {
+  std::mutex mu;
+  bool enabled = false;
+  struct Rec { int kind; hipEvent_t a, b; };
+  std::vector<Rec> pending;
+  std::vector<hipEvent_t> free_events;
+
+  hipEvent_t get() {
+    if (!free_events.empty()) {
+      hipEvent_t e = free_events.back();
+      free_events.pop_back();
+      return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+  }
+};
+Profiler g_prof;
+
+// Brackets one kernel launch with events when profiling is on.
+class ProfScope {
+ public:
+  ProfScope(int kind, hipStream_t s, bool active) : kind_(kind), s_(s) {
+    if (!active) return;
+    std::lock_guard<std::mutex> lk(g_prof.mu);
+    if (!g_prof.enabled) return;
+    a_ = g_prof.get();
+    b_ = g_prof.get();
+    if (a_ && b_ && hipEventRecord(a_, s_) == hipSuccess) return;
+    release();
+  }
+  ~ProfScope() {
+    if (!a_) return;
+    std::lock_guard<std::mutex> lk(g_prof.mu);
+    if (hipEventRecord(b_, s_) == hipSuccess) {
+      g_prof.pending.push_back({kind_, a_, b_});
+    } else {
+      release();
+    }
+  }
+
+ private:
+  void release() {
+    if (a_) g_prof.free_events.push_back(a_);
+    if (b_) g_prof.free_events.push_back(b_);
+    a_ = b_ = nullptr;
+  }
+  int kind_;
+  hipStream_t s_;
+  hipEvent_t a_ = nullptr, b_ = nullptr;
+};
 
 libra_status check_layout(const libra_kv_layout_desc* d) {
   if (!d) return set_error(LIBRA_E_INVAL, "layout descriptor is NULL");
@@ -83,13 +139,16 @@ libra_status upload(Plan& P, void* ws, size_t ws_bytes, hipStream_t s) {
       return hip_error(e, "hipEventCreate");
     }
   }
-  if (P.upload_bytes > 0) {
-    e = hipMemcpyAsync(ws, P.pinned, P.upload_bytes, hipMemcpyHostToDevice, s);
-    if (e != hipSuccess) return hip_error(e, "hipMemcpyAsync(plan tables)");
+  {
+    ProfScope ps(LIBRA_KERNEL_UPLOAD, s, true);
+    if (P.upload_bytes > 0) {
+      e = hipMemcpyAsync(ws, P.pinned, P.upload_bytes, hipMemcpyHostToDevice, s);
+      if (e != hipSuccess) return hip_error(e, "hipMemcpyAsync(plan tables)");
+    }
+    e = launch_zero_i32(reinterpret_cast<int32_t*>(static_cast<char*>(ws) + P.off_counters),
+                        P.n_counters, s);
+    if (e != hipSuccess) return hip_error(e, "zero counters");
   }
-  e = launch_zero_i32(reinterpret_cast<int32_t*>(static_cast<char*>(ws) + P.off_counters),
-                      P.n_counters, s);
-  if (e != hipSuccess) return hip_error(e, "zero counters");
   e = hipEventRecord(P.upload_done, s);
   if (e != hipSuccess) return hip_error(e, "hipEventRecord");
   P.uploaded_ws = ws;
@@ -119,6 +178,28 @@ libra_status check_call(const KvLayout* L, const Plan* P, int mode, const void* 
       return set_error(LIBRA_E_INVAL, "bt_stride smaller than the pages the plan's lengths need");
   }
   return LIBRA_OK;
+}
+
+// Decode units, chunk units, then the merge of split rows, on one stream.
+libra_status launch_attention(const KvLayout& L, const Plan& P, void* ws, const void* q,
+                              const int32_t* bt, int32_t stride, float scale, void* out,
+                              float* lse, hipStream_t s) {
+  hipError_t e;
+  {
+    ProfScope ps(LIBRA_KERNEL_DECODE, s, P.info.n_single > 0);
+    e = launch_decode(L, P, ws, q, bt, stride, scale, out, lse, s);
+  }
+  if (e != hipSuccess) return hip_error(e, "decode launch");
+  {
+    ProfScope ps(LIBRA_KERNEL_CHUNK, s, P.info.n_chunk > 0);
+    e = launch_chunk(L, P, ws, q, bt, stride, scale, out, lse, s);
+  }
+  if (e != hipSuccess) return hip_error(e, "chunk launch");
+  {
+    ProfScope ps(LIBRA_KERNEL_MERGE, s, merge_launches(P));
+    e = launch_merge(P, ws, out, lse, s);
+  }
+  return e == hipSuccess ? LIBRA_OK : hip_error(e, "merge launch");
 }
 
 }  // namespace
@@ -167,8 +248,11 @@ libra_status libra_kv_pack_pages(libra_kv_layout layout, const void* k_src, cons
     return set_error(LIBRA_E_INVAL, "page range outside the cache");
   if ((k_src && !aligned16(k_src)) || (v_src && !aligned16(v_src)))
     return set_error(LIBRA_E_INVAL, "sources must be 16-byte aligned");
-  hipError_t e = launch_pack(*layout, k_src, v_src, first_page, n_pages,
-                             static_cast<hipStream_t>(stream));
+  hipError_t e;
+  {
+    ProfScope ps(LIBRA_KERNEL_PACK, static_cast<hipStream_t>(stream), n_pages > 0);
+    e = launch_pack(*layout, k_src, v_src, first_page, n_pages, static_cast<hipStream_t>(stream));
+  }
   return e == hipSuccess ? LIBRA_OK : hip_error(e, "pack launch");
 }
 
@@ -180,8 +264,11 @@ libra_status libra_kv_unpack_pages(libra_kv_layout layout, void* k_dst, void* v_
     return set_error(LIBRA_E_INVAL, "page range outside the cache");
   if ((k_dst && !aligned16(k_dst)) || (v_dst && !aligned16(v_dst)))
     return set_error(LIBRA_E_INVAL, "destinations must be 16-byte aligned");
-  hipError_t e = launch_unpack(*layout, k_dst, v_dst, first_page, n_pages,
-                               static_cast<hipStream_t>(stream));
+  hipError_t e;
+  {
+    ProfScope ps(LIBRA_KERNEL_UNPACK, static_cast<hipStream_t>(stream), n_pages > 0);
+    e = launch_unpack(*layout, k_dst, v_dst, first_page, n_pages, static_cast<hipStream_t>(stream));
+  }
   return e == hipSuccess ? LIBRA_OK : hip_error(e, "unpack launch");
 }
 
@@ -198,8 +285,12 @@ libra_status libra_kv_gather(libra_kv_layout layout, const int32_t* block_table,
     return set_error(LIBRA_E_UNSUPPORTED, "batch and num_kv_heads must be <= 65535");
   if (!aligned16(k_out) || !aligned16(v_out))
     return set_error(LIBRA_E_INVAL, "outputs must be 16-byte aligned");
-  hipError_t e = launch_gather(*layout, block_table, bt_stride, cu_seq_lens, batch, max_pages,
-                               k_out, v_out, static_cast<hipStream_t>(stream));
+  hipError_t e;
+  {
+    ProfScope ps(LIBRA_KERNEL_GATHER, static_cast<hipStream_t>(stream), true);
+    e = launch_gather(*layout, block_table, bt_stride, cu_seq_lens, batch, max_pages, k_out, v_out,
+                      static_cast<hipStream_t>(stream));
+  }
   return e == hipSuccess ? LIBRA_OK : hip_error(e, "gather launch");
 }
 
@@ -299,11 +390,7 @@ libra_status libra_decode_attn(libra_kv_layout layout, libra_plan plan, const vo
     st = upload(*plan, workspace, ws_bytes, s);
     if (st != LIBRA_OK) return st;
   }
-  hipError_t e = launch_decode(*layout, *plan, workspace, q, block_table, bt_stride, scale, out,
-                               lse, s);
-  if (e != hipSuccess) return hip_error(e, "decode launch");
-  e = launch_merge(*plan, workspace, out, lse, s);
-  return e == hipSuccess ? LIBRA_OK : hip_error(e, "merge launch");
+  return launch_attention(*layout, *plan, workspace, q, block_table, bt_stride, scale, out, lse, s);
 }
 
 libra_status libra_append_attn(libra_kv_layout layout, libra_plan plan, const void* q,
@@ -326,15 +413,38 @@ libra_status libra_append_attn(libra_kv_layout layout, libra_plan plan, const vo
     st = upload(*plan, workspace, ws_bytes, s);
     if (st != LIBRA_OK) return st;
   }
-  hipError_t e = launch_cache_write(*layout, *plan, workspace, k_new, v_new, block_table,
-                                    bt_stride, s);
+  hipError_t e;
+  {
+    ProfScope ps(LIBRA_KERNEL_CACHE_WRITE, s, plan->info.n_write_tiles > 0);
+    e = launch_cache_write(*layout, *plan, workspace, k_new, v_new, block_table, bt_stride, s);
+  }
   if (e != hipSuccess) return hip_error(e, "cache-write launch");
-  e = launch_decode(*layout, *plan, workspace, q, block_table, bt_stride, scale, out, lse, s);
-  if (e != hipSuccess) return hip_error(e, "decode launch");
-  e = launch_chunk(*layout, *plan, workspace, q, block_table, bt_stride, scale, out, lse, s);
-  if (e != hipSuccess) return hip_error(e, "chunk launch");
-  e = launch_merge(*plan, workspace, out, lse, s);
-  return e == hipSuccess ? LIBRA_OK : hip_error(e, "merge launch");
+  return launch_attention(*layout, *plan, workspace, q, block_table, bt_stride, scale, out, lse, s);
+}
+
+libra_status libra_profile_enable(int enable) {
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  g_prof.enabled = enable != 0;
+  return LIBRA_OK;
+}
+
+libra_status libra_profile_collect(libra_kernel_times* out) {
+  if (!out) return set_error(LIBRA_E_INVAL, "out is NULL");
+  std::memset(out, 0, sizeof(*out));
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  libra_status st = LIBRA_OK;
+  for (const Profiler::Rec& r : g_prof.pending) {
+    float ms = 0.f;
+    hipError_t e = hipEventSynchronize(r.b);
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, r.a, r.b);
+    if (e != hipSuccess && st == LIBRA_OK) st = hip_error(e, "reading kernel timing events");
+    out->ms[r.kind] += ms;
+    out->launches[r.kind] += 1;
+    g_prof.free_events.push_back(r.a);
+    g_prof.free_events.push_back(r.b);
+  }
+  g_prof.pending.clear();
+  return st;
 }
 
 }  // extern "C"

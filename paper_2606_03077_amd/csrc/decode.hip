@@ -469,9 +469,11 @@ hipError_t launch_decode(const KvLayout& L, const Plan& P, void* ws, const void*
 
 namespace libra {
 
+bool merge_launches(const Plan& P) { return P.info.n_merge_groups > 0 && !LIBRA_FUSED_MERGE; }
+
 hipError_t launch_merge(const Plan& P, void* ws, void* out, float* lse, hipStream_t s) {
   const int n = P.info.n_merge_groups;
-  if (n == 0 || LIBRA_FUSED_MERGE) return hipSuccess;
+  if (!merge_launches(P)) return hipSuccess;
   char* w = static_cast<char*>(ws);
   MergeArgs A;
   A.merges = reinterpret_cast<const int32_t*>(w + P.off_merges);

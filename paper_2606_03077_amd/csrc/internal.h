@@ -82,6 +82,7 @@ hipError_t launch_decode(const KvLayout& L, const Plan& P, void* ws, const void*
                          hipStream_t s);
 hipError_t launch_zero_i32(int32_t* p, int64_t n, hipStream_t s);
 hipError_t launch_merge(const Plan& P, void* ws, void* out, float* lse, hipStream_t s);
+bool merge_launches(const Plan& P);  // whether launch_merge enqueues a kernel for P
 hipError_t launch_chunk(const KvLayout& L, const Plan& P, void* ws, const void* q,
                         const int32_t* bt, int32_t stride, float scale, void* out, float* lse,
                         hipStream_t s);

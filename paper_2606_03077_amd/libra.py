@@ -32,7 +32,9 @@ EXPORTS = ("libra_status_string", "libra_last_error", "libra_kv_layout_create",
            "libra_kv_layout_destroy", "libra_kv_pack_pages", "libra_kv_unpack_pages",
            "libra_kv_gather", "libra_splitkv_plan", "libra_plan_get_units", "libra_plan_get_info",
            "libra_plan_workspace_bytes", "libra_plan_upload", "libra_plan_destroy",
-           "libra_decode_attn", "libra_append_attn")
+           "libra_decode_attn", "libra_append_attn", "libra_profile_enable",
+           "libra_profile_collect")
+KERNEL_KINDS = ("pack", "unpack", "gather", "cache_write", "decode", "merge", "chunk", "upload")
 
 
 class LibraError(RuntimeError):
@@ -65,6 +67,11 @@ class PlanInfo(ctypes.Structure):
                 ("chunk_pages", ctypes.c_int64), ("q_tile", ctypes.c_int32),
                 ("n_rows", ctypes.c_int32), ("n_write_tiles", ctypes.c_int32),
                 ("num_cus", ctypes.c_int32), ("n_merge_groups", ctypes.c_int32)]
+
+
+class KernelTimes(ctypes.Structure):
+    _fields_ = [("ms", ctypes.c_double * len(KERNEL_KINDS)),
+                ("launches", ctypes.c_int64 * len(KERNEL_KINDS))]
 
 
 _lib = None
@@ -104,6 +111,8 @@ def load() -> ctypes.CDLL:
                                              P, P, P]),
         "libra_append_attn": (ctypes.c_int, [P, P, P, P, P, P, I32, I32, I32, ctypes.c_float, P,
                                              SZ, P, P, P]),
+        "libra_profile_enable": (ctypes.c_int, [ctypes.c_int]),
+        "libra_profile_collect": (ctypes.c_int, [ctypes.POINTER(KernelTimes)]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -250,6 +259,17 @@ def libra_append_attn(layout: int, plan: int, q, k_new, v_new, block_table, bt_s
                                     _ptr(block_table), bt_stride, batch, num_q_heads, scale,
                                     _ptr(workspace), ws_bytes, _ptr(out), _ptr(lse),
                                     _stream(stream)), "libra_append_attn")
+
+
+def libra_profile_enable(enable: bool = True) -> None:
+    _check(load().libra_profile_enable(1 if enable else 0), "libra_profile_enable")
+
+
+def libra_profile_collect() -> dict:
+    """{kind: (total_ms, launches)} accumulated since the last collect."""
+    t = KernelTimes()
+    _check(load().libra_profile_collect(ctypes.byref(t)), "libra_profile_collect")
+    return {k: (t.ms[i], t.launches[i]) for i, k in enumerate(KERNEL_KINDS)}
 
 
 def alloc_workspace(plan: int, device="cuda") -> torch.Tensor:
