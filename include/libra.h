@@ -143,8 +143,13 @@ libra_status libra_kv_gather(libra_kv_layout layout, const int32_t* block_table,
  *    if q_tile = 0): tile k holds new tokens [kT, min(kT + T, C_b)) and keys
  *    [0, P_b + min(kT + T, C_b)), P_b = L_b - C_b.  Tiles are not split along KV.
  * 6. Every unit is repeated for each KV head g.
- * 7. Single units come first, by descending KV tokens, ties by ascending (b, g, j);
- *    then chunk units by descending KV tokens x query tokens, ties by (b, g, q_begin).
+ * 7. Single units come first, by descending KV tokens, ties by ascending (b, g, j).
+ *    Chunk units follow, grouped per (b, g) and dealt to 8 per-XCD queues: a tile costs
+ *    KV tokens x query tokens, a group the sum of its tiles; groups by descending cost
+ *    (ties ascending (b, g)) go to the queue with the least accumulated cost (ties to the
+ *    lowest queue); within a group, tiles by descending cost, ties ascending q_begin;
+ *    queue 0's tiles are listed first, then queue 1's, ... (the chunk launch runs queue
+ *    x's tiles on workgroups w with w % 8 = x, so all tiles of a group share an L2).
  * 8. Single rows with n_b > 1 own n_b float32 partial-result slots per KV head,
  *    allotted in ascending (b, g): part_base(b, g) = earlier split rows' slots + g n_b.
  *

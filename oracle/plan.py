@@ -28,9 +28,12 @@ units per CU, minimum split size in pages, maximum splits, chunk query tile).
    when q_tile = 0): tile k holds new tokens [kT, min(kT + T, C_b)) and keys
    [0, P_b + min(kT + T, C_b)), where P_b = L_b - C_b.  Tiles are not split along KV.
 6. Every unit is repeated for each KV head g.
-7. Single units are ordered by descending KV token count, ties by ascending (b, g, j);
-   chunk units by descending (KV tokens x query tokens), ties by ascending (b, g, q_begin).
-   The table lists all single units, then all chunk units.
+7. Single units are ordered by descending KV token count, ties by ascending (b, g, j).
+   Chunk units are grouped per (b, g); a tile costs KV tokens x query tokens and a group
+   the sum of its tiles.  Groups, by descending cost (ties ascending (b, g)), are dealt to
+   8 queues (one per XCD), each to the queue with the least accumulated cost (ties to the
+   lowest queue).  Within a group, tiles go by descending cost, ties ascending q_begin.
+   The table lists all single units, then queue 0's tiles, queue 1's, ... queue 7's.
 8. Single rows with n_b > 1 own n_b partial-result slots per KV head, allotted in
    ascending (b, g) order: part_base(b, g) = (slots of earlier split rows) + g * n_b.
    Units with n_b = 1 have part_base = -1.
@@ -46,6 +49,7 @@ UNIT_FIELDS = ("b", "g", "kv_begin", "kv_end", "q_begin", "q_end", "split", "n_s
 KIND_SINGLE = 0
 KIND_CHUNK = 1
 PAGE = 16
+NUM_XCDS = 8
 
 
 @dataclasses.dataclass(frozen=True)
@@ -114,8 +118,22 @@ def plan_ref(seq_lens, q_lens, num_kv_heads: int, group: int, params: PlanParams
                 q0 = k * T
                 q1 = min(q0 + T, C[b])
                 chunks.append((b, g, 0, P + q1, q0, q1, 0, 1, -1, row0[b], KIND_CHUNK, P))
-    chunks.sort(key=lambda u: (-(u[3] - u[2]) * (u[5] - u[4]), u[0], u[1], u[4]))
+    def cost(u):
+        return (u[3] - u[2]) * (u[5] - u[4])
+
+    groups = {}
+    for u in chunks:
+        groups.setdefault((u[0], u[1]), []).append(u)
+    order = sorted(groups, key=lambda k: (-sum(cost(u) for u in groups[k]), k[0], k[1]))
+    queues = [[] for _ in range(NUM_XCDS)]
+    qcost = [0] * NUM_XCDS
+    for k in order:
+        x = min(range(NUM_XCDS), key=lambda i: (qcost[i], i))
+        qcost[x] += sum(cost(u) for u in groups[k])
+        queues[x].extend(sorted(groups[k], key=lambda u: (-cost(u), u[4])))
+    chunks = [u for q in queues for u in q]
 
     info = {"n_single": len(singles), "n_chunk": len(chunks), "n_partial_slots": slots,
-            "chunk_pages": chunk, "q_tile": T, "work_pages": W}
+            "chunk_pages": chunk, "q_tile": T, "work_pages": W,
+            "xcd_queue_lens": [len(q) for q in queues]}
     return singles + chunks, info

@@ -131,6 +131,7 @@ libra_status upload(Plan& P, void* ws, size_t ws_bytes, hipStream_t s) {
     std::memcpy(h + P.off_units, P.units.data(), P.units.size() * sizeof(int32_t));
     std::memcpy(h + P.off_writes, P.writes.data(), P.writes.size() * sizeof(int32_t));
     std::memcpy(h + P.off_merges, P.merges.data(), P.merges.size() * sizeof(int32_t));
+    std::memcpy(h + P.off_xcd_map, P.xcd_map.data(), P.xcd_map.size() * sizeof(int32_t));
   }
   if (!P.upload_done) {
     e = hipEventCreateWithFlags(&P.upload_done, hipEventDisableTiming);

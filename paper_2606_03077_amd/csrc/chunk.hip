@@ -1,17 +1,21 @@
 // Causal attention of an appended chunk (e.g. a tool output) over the paged KV cache.
 //
-// One 256-thread workgroup per chunk unit (sequence b, KV head g, new tokens [q0, q1)).
-// Query rows are (token, head) pairs of the G heads sharing KV head g; they are packed
-// into 16-wide matrix columns, tpb = max(1, 16 / G) tokens per column block.  Each of
-// the 4 waves owns 4 column blocks (64 columns), so a workgroup covers up to 16 * tpb
-// tokens.  Keys are visited one page pair at a time; the pair's four 4 KiB tiles (K and
-// V of both pages) are staged in LDS, double-buffered, and shared by the 4 waves:
-// every K/V byte fetched from HBM feeds 64 query columns per wave.  The math per pair
-// and column block is the decode kernel's:
-//   S^T = K . Q^T (4 mfma 16x16x32 per page), online softmax in base 2,
-//   O^T += V^T . P^T (8 mfma 16x16x32 over the 32 keys of the pair).
-// Column c of block nb in wave w is token q0 + (4 w + nb) * tpb + c / G, head c % G; it
-// sees keys k <= P_b + token (causal, itself included).
+// One 512-thread workgroup (8 waves) per chunk unit (sequence b, KV head g, new tokens
+// [q0, q1)).  Query rows are (token, head) pairs of the G heads sharing KV head g, packed
+// into 16-wide matrix columns, tpb = max(1, 16 / G) tokens per column block; each wave
+// owns 2 column blocks, so a workgroup covers up to 16 * tpb tokens.  Keys are visited
+// 64 at a time: the step's eight 4 KiB tiles (K and V of 4 pages) are staged in LDS,
+// double-buffered, and shared by the 8 waves.  Per page and column block:
+//   S^T = K . Q^T (4 mfma 16x16x32), and per page pair O^T += V^T . P^T (8 mfma 16x16x32
+//   over 32 keys).
+// Softmax runs online in base 2.  The running maximum is only moved (and the
+// accumulators rescaled) when a step's scores exceed it by more than 2^kTau, which a
+// wave-wide vote detects; otherwise probabilities are taken against the old maximum
+// (at most 2^kTau, exact in the final normalisation).  Causal masks are applied only on
+// steps that reach past the tile's first token.  Column c of block nb in wave w is
+// token q0 + (2 w + nb) * tpb + c / G, head c % G, and sees keys k <= P_b + token.
+// Units arrive in per-XCD queues: workgroup w takes tile w / 8 of queue w % 8, so the
+// tiles of one (b, g), which read the same keys, run on one XCD and share its L2.
 #include <cmath>
 
 #include "internal.h"
@@ -22,10 +26,11 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kWaves = 4;
+constexpr int kWaves = 8;
 constexpr int kThreads = 64 * kWaves;
-constexpr int kNB = 4;               // column blocks per wave
-constexpr int kTileU4 = kTileBytes / 16;  // uint4 per tile (256)
+constexpr int kNB = 2;           // column blocks per wave
+constexpr int kStepPages = 4;    // pages (16 keys each) per softmax step
+constexpr float kTau = 8.f;      // lazy-rescale threshold, base-2 logits
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
@@ -37,10 +42,26 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return uint32_t(__builtin_bit_cast(uint16_t, a)) | (uint32_t(__builtin_bit_cast(uint16_t, b)) << 16);
 }
 
+// Zero V of the slots of this lane's quad at or beyond `valid` keys of the page.
+__device__ __forceinline__ void clear_v(uint4 (&v)[4], int quad, int valid) {
+  const int keep = min(max(valid - 4 * quad, 0), 4);
+  if (keep == 4) return;
+  const uint32_t m0 = keep >= 2 ? 0xFFFFFFFFu : (keep == 1 ? 0x0000FFFFu : 0u);
+  const uint32_t m1 = keep >= 4 ? 0xFFFFFFFFu : (keep == 3 ? 0x0000FFFFu : 0u);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    v[i].x &= m0;
+    v[i].y &= m1;
+    v[i].z &= m0;
+    v[i].w &= m1;
+  }
+}
+
 struct ChunkArgs {
   const uint16_t* k_cache;
   const uint16_t* v_cache;
-  const int32_t* units;
+  const int32_t* units;    // chunk units, queue by queue
+  const int32_t* xcd_map;  // (first unit, count) per XCD queue
   const int32_t* bt;
   const uint16_t* q;
   uint16_t* out;
@@ -52,11 +73,15 @@ struct ChunkArgs {
   float sl2;
 };
 
-__global__ __launch_bounds__(kThreads) void chunk_kernel(ChunkArgs A) {
-  // [buffer][KA, KB, VA, VB][256 x uint4]
-  __shared__ uint4 lds[2][4][kTileU4];
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void chunk_kernel(ChunkArgs A) {
+  // [buffer][page of the step][K, V][256 x uint4]
+  __shared__ uint4 lds[2][kStepPages][2][256];
 
-  const int32_t* u = A.units + size_t(blockIdx.x) * kUnitInts;
+  const int xcd = blockIdx.x % kNumXcds;
+  const int slot = blockIdx.x / kNumXcds;
+  if (slot >= A.xcd_map[2 * xcd + 1]) return;  // this queue is shorter than the longest
+  const int32_t* u = A.units + size_t(A.xcd_map[2 * xcd] + slot) * kUnitInts;
   const int b = u[U_B], g = u[U_G], kv1 = u[U_KV1];
   const int q0 = u[U_Q0], q1 = u[U_Q1], row0 = u[U_ROW0], prior = u[U_PRIOR];
 
@@ -65,11 +90,10 @@ __global__ __launch_bounds__(kThreads) void chunk_kernel(ChunkArgs A) {
   const int col = lane & 15, quad = lane >> 4;
   const int G = A.group;
   const int tpb = G >= 16 ? 1 : 16 / G;
+  const int head = col % G;
 
-  // Per column block: token, head, key limit and Q operand.
   int tok[kNB], lim[kNB];
   bf16x8 qop[kNB][4];
-  const int head = col % G;
 #pragma unroll
   for (int nb = 0; nb < kNB; ++nb) {
     const int t = q0 + (kNB * wave + nb) * tpb + col / G;
@@ -97,117 +121,135 @@ __global__ __launch_bounds__(kThreads) void chunk_kernel(ChunkArgs A) {
   }
 
   const int npages = (kv1 + kPage - 1) / kPage;
-  const int npairs = (npages + 1) >> 1;
+  const int nsteps = (npages + kStepPages - 1) / kStepPages;
   const int32_t* btrow = A.bt + int64_t(b) * A.bt_stride;
   const size_t head_off = size_t(g) * kTileElems;
   const size_t page_stride = size_t(A.hkv) * kTileElems;
+  const int half = tid >> 8;          // 0: this thread stages K tiles, 1: V tiles
+  const int elem = tid & 255;         // uint4 index inside a tile
+  const uint16_t* src_cache = half ? A.v_cache : A.k_cache;
+  const int first_tok = prior + q0;   // smallest query position of the tile
 
-  auto fetch = [&](int pair, uint4 (&r)[4]) {
-    const int pa = 2 * pair;
-    const size_t ba = size_t(btrow[pa]) * page_stride + head_off;
-    r[0] = reinterpret_cast<const uint4*>(A.k_cache + ba)[tid];
-    r[2] = reinterpret_cast<const uint4*>(A.v_cache + ba)[tid];
-    if (pa + 1 < npages) {
-      const size_t bb = size_t(btrow[pa + 1]) * page_stride + head_off;
-      r[1] = reinterpret_cast<const uint4*>(A.k_cache + bb)[tid];
-      r[3] = reinterpret_cast<const uint4*>(A.v_cache + bb)[tid];
-    } else {
-      r[1] = make_uint4(0, 0, 0, 0);
-      r[3] = make_uint4(0, 0, 0, 0);
+  // Thread t stages uint4 `elem` of the K (t < 256) or V tile of each page of a step.
+  auto fetch = [&](int step, uint4 (&r)[kStepPages]) {
+#pragma unroll
+    for (int j = 0; j < kStepPages; ++j) {
+      const int p = step * kStepPages + j;
+      if (p < npages) {
+        const size_t base = size_t(btrow[p]) * page_stride + head_off;
+        r[j] = reinterpret_cast<const uint4*>(src_cache + base)[elem];
+      } else {
+        r[j] = make_uint4(0, 0, 0, 0);
+      }
     }
   };
-  auto stash = [&](int buf, const uint4 (&r)[4]) {
+  auto stash = [&](int buf, const uint4 (&r)[kStepPages]) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) lds[buf][i][tid] = r[i];
+    for (int j = 0; j < kStepPages; ++j) lds[buf][j][half][elem] = r[j];
   };
 
-  uint4 stage[4];
-  if (npairs > 0) {
+  uint4 stage[kStepPages];
+  if (nsteps > 0) {
     fetch(0, stage);
     stash(0, stage);
   }
   __syncthreads();
 
-  for (int n = 0; n < npairs; ++n) {
+  for (int n = 0; n < nsteps; ++n) {
     const int buf = n & 1;
-    if (n + 1 < npairs) fetch(n + 1, stage);
+    if (n + 1 < nsteps) fetch(n + 1, stage);
+    const int key0 = n * kStepPages * kPage;
+    const bool masked = key0 + kStepPages * kPage - 1 > first_tok || key0 + kStepPages * kPage > kv1;
 
-    // This pair's operands, read from LDS in the same lane order as the tiles.
-    uint4 ka[4], kb[4], va[4], vb[4];
+    // Scores of the step's 4 pages for both column blocks.
+    f32x4 s[kStepPages][kNB];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      ka[i] = lds[buf][0][i * 64 + lane];
-      kb[i] = lds[buf][1][i * 64 + lane];
-      va[i] = lds[buf][2][i * 64 + lane];
-      vb[i] = lds[buf][3][i * 64 + lane];
-    }
-    const int key_a = 2 * n * kPage;  // first key of page A
-    // Zero V of slots at or past kv1 (never-written or NaN-poisoned slots).
-    if (key_a + 2 * kPage > kv1) {
+    for (int j = 0; j < kStepPages; ++j) {
+      uint4 kr[4];
 #pragma unroll
-      for (int pgi = 0; pgi < 2; ++pgi) {
-        const int keep = min(max(kv1 - key_a - pgi * kPage - 4 * quad, 0), 4);
-        const uint32_t m0 = keep >= 2 ? 0xFFFFFFFFu : (keep == 1 ? 0x0000FFFFu : 0u);
-        const uint32_t m1 = keep >= 4 ? 0xFFFFFFFFu : (keep == 3 ? 0x0000FFFFu : 0u);
+      for (int i = 0; i < 4; ++i) kr[i] = lds[buf][j][0][i * 64 + lane];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          uint4& v = pgi == 0 ? va[i] : vb[i];
-          v.x &= m0;
-          v.y &= m1;
-          v.z &= m0;
-          v.w &= m1;
-        }
+      for (int nb = 0; nb < kNB; ++nb) {
+        f32x4 a = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kr[i]), qop[nb][i], a, 0, 0, 0);
+        s[j][nb] = a;
       }
     }
 
+    bf16x8 pop[kNB][2];
 #pragma unroll
     for (int nb = 0; nb < kNB; ++nb) {
-      f32x4 sa = {0.f, 0.f, 0.f, 0.f}, sb = {0.f, 0.f, 0.f, 0.f};
+      if (masked) {
+#pragma unroll
+        for (int j = 0; j < kStepPages; ++j)
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (key0 + j * kPage + 4 * quad + r > lim[nb]) s[j][nb][r] = -INFINITY;
+      }
+      float mloc = -INFINITY;
+#pragma unroll
+      for (int j = 0; j < kStepPages; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) mloc = fmaxf(mloc, s[j][nb][r]);
+      const float xmax = mloc * A.sl2;
+      if (__ballot(xmax > m[nb] + kTau)) {  // wave-uniform, rare after the first steps
+        float mc = fmaxf(xmax, m[nb]);
+        mc = fmaxf(mc, __shfl_xor(mc, 16));
+        mc = fmaxf(mc, __shfl_xor(mc, 32));
+        const float alpha = m[nb] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m[nb] - mc);
+        l[nb] *= alpha;
+#pragma unroll
+        for (int db = 0; db < 8; ++db) acc[nb][db] *= alpha;
+        m[nb] = mc;
+      }
+      const float neg_m = m[nb] == -INFINITY ? 0.f : -m[nb];
+      float p[kStepPages][4];
+      float ps = 0.f;
+#pragma unroll
+      for (int j = 0; j < kStepPages; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          p[j][r] = __builtin_amdgcn_exp2f(fmaf(s[j][nb][r], A.sl2, neg_m));
+          ps += p[j][r];
+        }
+      l[nb] += ps;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        uint4 pb;
+        pb.x = pack_bf16x2(p[2 * h][0], p[2 * h][1]);
+        pb.y = pack_bf16x2(p[2 * h][2], p[2 * h][3]);
+        pb.z = pack_bf16x2(p[2 * h + 1][0], p[2 * h + 1][1]);
+        pb.w = pack_bf16x2(p[2 * h + 1][2], p[2 * h + 1][3]);
+        pop[nb][h] = as_bf16x8(pb);
+      }
+    }
+
+    // O^T += V^T P^T over each page pair (32 keys).
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      uint4 va[4], vb[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        sa = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(ka[i]), qop[nb][i], sa, 0, 0, 0);
-        sb = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kb[i]), qop[nb][i], sb, 0, 0, 0);
+        va[i] = lds[buf][2 * h][1][i * 64 + lane];
+        vb[i] = lds[buf][2 * h + 1][1][i * 64 + lane];
       }
-      float x[8];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int ka_pos = key_a + 4 * quad + r;
-        x[r] = ka_pos <= lim[nb] ? sa[r] * A.sl2 : -INFINITY;
-        x[4 + r] = ka_pos + kPage <= lim[nb] ? sb[r] * A.sl2 : -INFINITY;
+      if (key0 + (2 * h + 2) * kPage > kv1) {  // slots at or past kv1 may hold NaN
+        clear_v(va, quad, kv1 - key0 - 2 * h * kPage);
+        clear_v(vb, quad, kv1 - key0 - (2 * h + 1) * kPage);
       }
-      float mx = x[0];
-#pragma unroll
-      for (int i = 1; i < 8; ++i) mx = fmaxf(mx, x[i]);
-      mx = fmaxf(mx, __shfl_xor(mx, 16));
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float m_new = fmaxf(m[nb], mx);
-      const float m_use = m_new == -INFINITY ? 0.f : m_new;
-      const float alpha = __builtin_amdgcn_exp2f(m[nb] - m_use);
-      float p[8], ps = 0.f;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        p[i] = __builtin_amdgcn_exp2f(x[i] - m_use);
-        ps += p[i];
-      }
-      l[nb] = l[nb] * alpha + ps;
-      m[nb] = m_new;
-      uint4 pb;
-      pb.x = pack_bf16x2(p[0], p[1]);
-      pb.y = pack_bf16x2(p[2], p[3]);
-      pb.z = pack_bf16x2(p[4], p[5]);
-      pb.w = pack_bf16x2(p[6], p[7]);
-      const bf16x8 pop = as_bf16x8(pb);
 #pragma unroll
       for (int db = 0; db < 8; ++db) {
         const uint4 a4 = va[db >> 1], b4 = vb[db >> 1];
         const uint4 vo = (db & 1) ? make_uint4(a4.z, a4.w, b4.z, b4.w)
                                   : make_uint4(a4.x, a4.y, b4.x, b4.y);
-        acc[nb][db] *= alpha;
-        acc[nb][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(vo), pop, acc[nb][db], 0, 0, 0);
+#pragma unroll
+        for (int nb = 0; nb < kNB; ++nb)
+          acc[nb][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(vo), pop[nb][h], acc[nb][db], 0, 0, 0);
       }
     }
 
-    if (n + 1 < npairs) stash(buf ^ 1, stage);
+    if (n + 1 < nsteps) stash(buf ^ 1, stage);
     __syncthreads();
   }
 
@@ -238,13 +280,13 @@ __global__ __launch_bounds__(kThreads) void chunk_kernel(ChunkArgs A) {
 hipError_t launch_chunk(const KvLayout& L, const Plan& P, void* ws, const void* q,
                         const int32_t* bt, int32_t stride, float scale, void* out, float* lse,
                         hipStream_t s) {
-  const int n = P.info.n_chunk;
-  if (n == 0) return hipSuccess;
+  if (P.info.n_chunk == 0) return hipSuccess;
   char* w = static_cast<char*>(ws);
   ChunkArgs A;
   A.k_cache = static_cast<const uint16_t*>(L.desc.k_cache);
   A.v_cache = static_cast<const uint16_t*>(L.desc.v_cache);
   A.units = reinterpret_cast<const int32_t*>(w + P.off_units) + size_t(P.info.n_single) * kUnitInts;
+  A.xcd_map = reinterpret_cast<const int32_t*>(w + P.off_xcd_map);
   A.bt = bt;
   A.q = static_cast<const uint16_t*>(q);
   A.out = static_cast<uint16_t*>(out);
@@ -254,7 +296,7 @@ hipError_t launch_chunk(const KvLayout& L, const Plan& P, void* ws, const void* 
   A.hq = P.num_q_heads;
   A.group = P.group;
   A.sl2 = scale * kLog2e;
-  hipLaunchKernelGGL(chunk_kernel, dim3(unsigned(n)), dim3(kThreads), 0, s, A);
+  hipLaunchKernelGGL(chunk_kernel, dim3(unsigned(P.chunk_grid)), dim3(kThreads), 0, s, A);
   return hipGetLastError();
 }
 

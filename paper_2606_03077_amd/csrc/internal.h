@@ -23,6 +23,7 @@ enum UnitField : int {
 };
 constexpr int kKindSingle = 0;
 constexpr int kKindChunk = 1;
+constexpr int kNumXcds = 8;  // MI355X: workgroup w is dispatched to XCD w % 8
 
 // Append cache-write table: one record per (sequence, page) the new tokens touch.
 enum WriteField : int { W_B = 0, W_PAGE, W_SLOT0, W_SLOT1, W_ROW, W_PAD0, W_PAD1, W_PAD2 };
@@ -40,12 +41,14 @@ struct Plan {
   std::vector<int32_t> units;   // n_units * kUnitInts
   std::vector<int32_t> writes;  // n_write_tiles * kWriteInts (append only)
   std::vector<int32_t> merges;  // n_merge_groups * kMergeInts
+  std::vector<int32_t> xcd_map; // (first chunk unit, count) per XCD queue
+  int64_t chunk_grid = 0;       // workgroups of the chunk launch: kNumXcds * longest queue
 
-  // Workspace image: [units | writes | merges | counters | partial o | partial lse],
+  // Workspace image: [units | writes | merges | xcd map | counters | partial o | partial lse],
   // 256-B aligned.  Counters (one per sequence x KV head when any row is split) start at
   // zero after an upload and are returned to zero by the split merge.
-  size_t off_units = 0, off_writes = 0, off_merges = 0, off_counters = 0, off_part_o = 0,
-         off_part_lse = 0;
+  size_t off_units = 0, off_writes = 0, off_merges = 0, off_xcd_map = 0, off_counters = 0,
+         off_part_o = 0, off_part_lse = 0;
   int32_t n_counters = 0;
   size_t ws_bytes = 0;
   size_t upload_bytes = 0;  // bytes of [units | writes | merges] copied from the host

@@ -114,14 +114,54 @@ libra_status build_plan(const libra_plan_desc& d, const int32_t* seq_lens, const
       }
     }
   }
-  std::sort(chunks.begin(), chunks.end(), [](const Unit& x, const Unit& y) {
-    const int64_t cx = int64_t(x[U_KV1] - x[U_KV0]) * (x[U_Q1] - x[U_Q0]);
-    const int64_t cy = int64_t(y[U_KV1] - y[U_KV0]) * (y[U_Q1] - y[U_Q0]);
-    if (cx != cy) return cx > cy;
+  // Step 7 (chunk units): XCD-affine order.  Tiles of one (b, g) read the same keys, so
+  // they are kept on one XCD (workgroup w runs on XCD w % kNumXcds) to share its L2.
+  // Groups by descending total cost (ties ascending (b, g)) are dealt to the XCD queue
+  // with the least accumulated cost (ties to the lowest queue); inside a group, tiles by
+  // descending cost, ties ascending q_begin; queues are listed one after another.
+  auto cost = [](const Unit& u) { return int64_t(u[U_KV1] - u[U_KV0]) * (u[U_Q1] - u[U_Q0]); };
+  std::vector<std::pair<size_t, size_t>> groups;  // [first, last) in chunks (built in (b, g) order)
+  for (size_t i = 0; i < chunks.size();) {
+    size_t j = i + 1;
+    while (j < chunks.size() && chunks[j][U_B] == chunks[i][U_B] && chunks[j][U_G] == chunks[i][U_G]) ++j;
+    groups.emplace_back(i, j);
+    i = j;
+  }
+  std::vector<int64_t> gcost(groups.size(), 0);
+  for (size_t k = 0; k < groups.size(); ++k)
+    for (size_t i = groups[k].first; i < groups[k].second; ++i) gcost[k] += cost(chunks[i]);
+  std::vector<size_t> gorder(groups.size());
+  for (size_t k = 0; k < gorder.size(); ++k) gorder[k] = k;
+  std::sort(gorder.begin(), gorder.end(), [&](size_t a, size_t b) {
+    if (gcost[a] != gcost[b]) return gcost[a] > gcost[b];
+    const Unit &x = chunks[groups[a].first], &y = chunks[groups[b].first];
     if (x[U_B] != y[U_B]) return x[U_B] < y[U_B];
-    if (x[U_G] != y[U_G]) return x[U_G] < y[U_G];
-    return x[U_Q0] < y[U_Q0];
+    return x[U_G] < y[U_G];
   });
+  std::vector<std::vector<Unit>> queues(kNumXcds);
+  int64_t qcost[kNumXcds] = {0};
+  for (size_t k : gorder) {
+    int x = 0;
+    for (int y = 1; y < kNumXcds; ++y)
+      if (qcost[y] < qcost[x]) x = y;
+    qcost[x] += gcost[k];
+    std::vector<Unit> tiles(chunks.begin() + groups[k].first, chunks.begin() + groups[k].second);
+    std::sort(tiles.begin(), tiles.end(), [&](const Unit& a, const Unit& b) {
+      const int64_t ca = cost(a), cb = cost(b);
+      if (ca != cb) return ca > cb;
+      return a[U_Q0] < b[U_Q0];
+    });
+    queues[x].insert(queues[x].end(), tiles.begin(), tiles.end());
+  }
+  chunks.clear();
+  int32_t xcd_map[2 * kNumXcds];
+  int32_t longest = 0;
+  for (int x = 0; x < kNumXcds; ++x) {
+    xcd_map[2 * x] = int32_t(chunks.size());
+    xcd_map[2 * x + 1] = int32_t(queues[x].size());
+    longest = std::max<int32_t>(longest, int32_t(queues[x].size()));
+    chunks.insert(chunks.end(), queues[x].begin(), queues[x].end());
+  }
 
   Plan& P = *out;
   P.mode = d.mode;
@@ -149,6 +189,9 @@ libra_status build_plan(const libra_plan_desc& d, const int32_t* seq_lens, const
       }
     }
   }
+
+  P.xcd_map.assign(xcd_map, xcd_map + 2 * kNumXcds);
+  P.chunk_grid = int64_t(kNumXcds) * longest;
 
   // Split-merge table: every single row with n_b > 1, per KV head, ascending (b, g).
   P.merges.clear();
@@ -182,6 +225,8 @@ libra_status build_plan(const libra_plan_desc& d, const int32_t* seq_lens, const
   off = align256(off + P.writes.size() * sizeof(int32_t));
   P.off_merges = off;
   off = align256(off + P.merges.size() * sizeof(int32_t));
+  P.off_xcd_map = off;
+  off = align256(off + P.xcd_map.size() * sizeof(int32_t));
   P.upload_bytes = off;
   P.n_counters = slots > 0 ? int32_t(B * Hkv) : 0;
   P.off_counters = off;

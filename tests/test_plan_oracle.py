@@ -26,19 +26,21 @@ def test_hand_derived_append_example():
     # L = [10, 100], C = [1, 70], Hkv = 2, G = 8 -> T = 16 * (16 // 8) = 32.
     # Single row 0: one page, W = 2, target = 4, chunk = 1, n = 1.
     # Chunk row 1: P = 30, tiles [0,32) [32,64) [64,70) with keys [0,62) [0,94) [0,100);
-    # costs 62*32 = 1984, 94*32 = 3008, 100*6 = 600.
+    # costs 62*32 = 1984, 94*32 = 3008, 100*6 = 600; both KV-head groups cost 5592, so
+    # (1, 0) goes to queue 0 and (1, 1) to queue 1, each listing its tiles 3008, 1984, 600.
     units, info = plan_ref([10, 100], [1, 70], 2, 8,
                            PlanParams(num_cus=4, units_per_cu=1, min_split_pages=1, max_splits=4))
     assert units == [
         (0, 0, 0, 10, 0, 1, 0, 1, -1, 0, 0, 9),
         (0, 1, 0, 10, 0, 1, 0, 1, -1, 0, 0, 9),
         (1, 0, 0, 94, 32, 64, 0, 1, -1, 1, 1, 30),
-        (1, 1, 0, 94, 32, 64, 0, 1, -1, 1, 1, 30),
         (1, 0, 0, 62, 0, 32, 0, 1, -1, 1, 1, 30),
-        (1, 1, 0, 62, 0, 32, 0, 1, -1, 1, 1, 30),
         (1, 0, 0, 100, 64, 70, 0, 1, -1, 1, 1, 30),
+        (1, 1, 0, 94, 32, 64, 0, 1, -1, 1, 1, 30),
+        (1, 1, 0, 62, 0, 32, 0, 1, -1, 1, 1, 30),
         (1, 1, 0, 100, 64, 70, 0, 1, -1, 1, 1, 30),
     ]
+    assert info["xcd_queue_lens"] == [3, 3, 0, 0, 0, 0, 0, 0]
     assert info["n_single"] == 2 and info["n_chunk"] == 6 and info["q_tile"] == 32
 
 
@@ -52,8 +54,32 @@ def check_invariants(seq_lens, q_lens, hkv, group, params):
     # ordering
     kv = [u[3] - u[2] for u in singles]
     assert kv == sorted(kv, reverse=True)
-    cost = [(u[3] - u[2]) * (u[5] - u[4]) for u in chunks]
-    assert cost == sorted(cost, reverse=True)
+    # chunk units: per-XCD queues, each (b, g) group contiguous inside one queue with its
+    # tiles by descending cost, groups dealt to the least-loaded queue
+    cost = lambda u: (u[3] - u[2]) * (u[5] - u[4])
+    lens = info["xcd_queue_lens"]
+    assert sum(lens) == len(chunks)
+    seen = set()
+    pos = 0
+    qcost = []
+    for n in lens:
+        q = chunks[pos:pos + n]
+        pos += n
+        qcost.append(sum(cost(u) for u in q))
+        i = 0
+        while i < len(q):
+            j = i
+            while j < len(q) and q[j][:2] == q[i][:2]:
+                j += 1
+            key = q[i][:2]
+            assert key not in seen
+            seen.add(key)
+            c = [cost(u) for u in q[i:j]]
+            assert c == sorted(c, reverse=True)
+            i = j
+    if chunks:
+        biggest_group = max(sum(cost(u) for u in chunks if u[:2] == k) for k in seen)
+        assert max(qcost) - min(qcost) <= biggest_group
     # single rows: splits tile [0, L) exactly, page aligned, non-empty unless L = 0
     slots = set()
     for b in range(B):
