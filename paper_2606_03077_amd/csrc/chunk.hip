@@ -5,7 +5,8 @@
 // into 16-wide matrix columns, tpb = max(1, 16 / G) tokens per column block; each wave
 // owns 2 column blocks, so a workgroup covers up to 16 * tpb tokens.  Keys are visited
 // 64 at a time: the step's eight 4 KiB tiles (K and V of 4 pages) are staged in LDS,
-// double-buffered, and shared by the 8 waves.  Per page and column block:
+// double-buffered, and shared by the 8 waves; V is interleaved by page pair on the way
+// in so that each PV operand is a single 16-byte LDS read.  Per page and column block:
 //   S^T = K . Q^T (4 mfma 16x16x32), and per page pair O^T += V^T . P^T (8 mfma 16x16x32
 //   over 32 keys).
 // Softmax runs online in base 2.  The running maximum is only moved (and the
@@ -31,6 +32,7 @@ constexpr int kThreads = 64 * kWaves;
 constexpr int kNB = 2;           // column blocks per wave
 constexpr int kStepPages = 4;    // pages (16 keys each) per softmax step
 constexpr float kTau = 8.f;      // lazy-rescale threshold, base-2 logits
+constexpr int kMaxIds = 4096;    // block-table entries staged in LDS (64K keys)
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
@@ -40,21 +42,6 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   const __bf16 a = static_cast<__bf16>(lo);
   const __bf16 b = static_cast<__bf16>(hi);
   return uint32_t(__builtin_bit_cast(uint16_t, a)) | (uint32_t(__builtin_bit_cast(uint16_t, b)) << 16);
-}
-
-// Zero V of the slots of this lane's quad at or beyond `valid` keys of the page.
-__device__ __forceinline__ void clear_v(uint4 (&v)[4], int quad, int valid) {
-  const int keep = min(max(valid - 4 * quad, 0), 4);
-  if (keep == 4) return;
-  const uint32_t m0 = keep >= 2 ? 0xFFFFFFFFu : (keep == 1 ? 0x0000FFFFu : 0u);
-  const uint32_t m1 = keep >= 4 ? 0xFFFFFFFFu : (keep == 3 ? 0x0000FFFFu : 0u);
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    v[i].x &= m0;
-    v[i].y &= m1;
-    v[i].z &= m0;
-    v[i].w &= m1;
-  }
 }
 
 struct ChunkArgs {
@@ -75,8 +62,13 @@ struct ChunkArgs {
 
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void chunk_kernel(ChunkArgs A) {
-  // [buffer][page of the step][K, V][256 x uint4]
-  __shared__ uint4 lds[2][kStepPages][2][256];
+  // K: [buffer][page of the step][256 x uint4], the tile as stored.
+  // V: [buffer][page pair][t][half][lane] x {page 2h bytes, page 2h+1 bytes}: for channel
+  // block db = 2 t + half, lane l's 16 bytes are exactly its PV A operand (4 slots of
+  // each page of the pair), so the PV loop reads operands with one ds_read_b128.
+  __shared__ uint4 ldk[2][kStepPages][256];
+  __shared__ uint2 ldv[2][kStepPages / 2][4][2][64][2];
+  __shared__ __align__(16) int lds_ids[kMaxIds];  // the tile's block-table row
 
   const int xcd = blockIdx.x % kNumXcds;
   const int slot = blockIdx.x / kNumXcds;
@@ -131,28 +123,57 @@ void chunk_kernel(ChunkArgs A) {
   const int first_tok = prior + q0;   // smallest query position of the tile
 
   // Thread t stages uint4 `elem` of the K (t < 256) or V tile of each page of a step.
+  // The step's 4 page ids come from LDS in one broadcast read; pages past the end
+  // re-read the last page (the id row is padded with it), so the loads stay branch-free
+  // and asynchronous; their keys are >= kv1, so they are masked and their V zeroed.
   auto fetch = [&](int step, uint4 (&r)[kStepPages]) {
+    const int p0 = step * kStepPages;
+    int ids[kStepPages];
+    if (p0 + kStepPages <= kMaxIds) {
+      const int4 v = *reinterpret_cast<const int4*>(&lds_ids[p0]);
+      ids[0] = v.x;
+      ids[1] = v.y;
+      ids[2] = v.z;
+      ids[3] = v.w;
+    } else {  // rows longer than the staged ids (uniform, rare)
+#pragma unroll
+      for (int j = 0; j < kStepPages; ++j)
+        ids[j] = __builtin_amdgcn_readfirstlane(btrow[min(p0 + j, npages - 1)]);
+    }
 #pragma unroll
     for (int j = 0; j < kStepPages; ++j) {
-      const int p = step * kStepPages + j;
-      if (p < npages) {
-        const size_t base = size_t(btrow[p]) * page_stride + head_off;
-        r[j] = reinterpret_cast<const uint4*>(src_cache + base)[elem];
-      } else {
-        r[j] = make_uint4(0, 0, 0, 0);
-      }
+      const size_t base = size_t(ids[j]) * page_stride + head_off;
+      r[j] = reinterpret_cast<const uint4*>(src_cache + base)[elem];
     }
   };
   auto stash = [&](int buf, const uint4 (&r)[kStepPages]) {
+    if (half == 0) {
 #pragma unroll
-    for (int j = 0; j < kStepPages; ++j) lds[buf][j][half][elem] = r[j];
+      for (int j = 0; j < kStepPages; ++j) ldk[buf][j][elem] = r[j];
+    } else {
+      const int t = elem >> 6, ln = elem & 63;
+#pragma unroll
+      for (int j = 0; j < kStepPages; ++j) {
+        ldv[buf][j >> 1][t][0][ln][j & 1] = make_uint2(r[j].x, r[j].y);
+        ldv[buf][j >> 1][t][1][ln][j & 1] = make_uint2(r[j].z, r[j].w);
+      }
+    }
   };
+
+  // Stage the page ids once (padded to whole steps with the last id), so that each
+  // prefetch is one dependent load, not two.
+  const int nids = min(nsteps * kStepPages, kMaxIds);
+  for (int i = tid; i < nids; i += kThreads) lds_ids[i] = btrow[min(i, npages - 1)];
+  __syncthreads();
 
   uint4 stage[kStepPages];
   if (nsteps > 0) {
     fetch(0, stage);
     stash(0, stage);
   }
+  // Every load issued so far (Q operands, the first stage) has landed: the loop's
+  // wait counts then only track the in-loop prefetch.
+  __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
 
   for (int n = 0; n < nsteps; ++n) {
@@ -167,7 +188,7 @@ void chunk_kernel(ChunkArgs A) {
     for (int j = 0; j < kStepPages; ++j) {
       uint4 kr[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) kr[i] = lds[buf][j][0][i * 64 + lane];
+      for (int i = 0; i < 4; ++i) kr[i] = ldk[buf][j][i * 64 + lane];
 #pragma unroll
       for (int nb = 0; nb < kNB; ++nb) {
         f32x4 a = {0.f, 0.f, 0.f, 0.f};
@@ -228,21 +249,26 @@ void chunk_kernel(ChunkArgs A) {
     // O^T += V^T P^T over each page pair (32 keys).
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-      uint4 va[4], vb[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        va[i] = lds[buf][2 * h][1][i * 64 + lane];
-        vb[i] = lds[buf][2 * h + 1][1][i * 64 + lane];
-      }
-      if (key0 + (2 * h + 2) * kPage > kv1) {  // slots at or past kv1 may hold NaN
-        clear_v(va, quad, kv1 - key0 - 2 * h * kPage);
-        clear_v(vb, quad, kv1 - key0 - (2 * h + 1) * kPage);
+      // Slots at or past kv1 may hold NaN: zero them in the operands of the last pages.
+      const bool tail = key0 + (2 * h + 2) * kPage > kv1;
+      uint32_t ma0 = ~0u, ma1 = ~0u, mb0 = ~0u, mb1 = ~0u;
+      if (tail) {
+        const int ka = min(max(kv1 - key0 - 2 * h * kPage - 4 * quad, 0), 4);
+        const int kb = min(max(kv1 - key0 - (2 * h + 1) * kPage - 4 * quad, 0), 4);
+        ma0 = ka >= 2 ? ~0u : (ka == 1 ? 0x0000FFFFu : 0u);
+        ma1 = ka >= 4 ? ~0u : (ka == 3 ? 0x0000FFFFu : 0u);
+        mb0 = kb >= 2 ? ~0u : (kb == 1 ? 0x0000FFFFu : 0u);
+        mb1 = kb >= 4 ? ~0u : (kb == 3 ? 0x0000FFFFu : 0u);
       }
 #pragma unroll
       for (int db = 0; db < 8; ++db) {
-        const uint4 a4 = va[db >> 1], b4 = vb[db >> 1];
-        const uint4 vo = (db & 1) ? make_uint4(a4.z, a4.w, b4.z, b4.w)
-                                  : make_uint4(a4.x, a4.y, b4.x, b4.y);
+        uint4 vo = *reinterpret_cast<const uint4*>(&ldv[buf][h][db >> 1][db & 1][lane][0]);
+        if (tail) {
+          vo.x &= ma0;
+          vo.y &= ma1;
+          vo.z &= mb0;
+          vo.w &= mb1;
+        }
 #pragma unroll
         for (int nb = 0; nb < kNB; ++nb)
           acc[nb][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(vo), pop[nb][h], acc[nb][db], 0, 0, 0);

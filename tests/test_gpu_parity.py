@@ -224,3 +224,15 @@ def test_split_merge_sees_fresh_partials_when_workspace_is_reused():
     for c in caches:
         c.close()
     libra.libra_plan_destroy(plan)
+
+
+def test_append_prior_longer_than_staged_block_table():
+    """A chunk whose keys span more pages than the chunk kernel stages in LDS (4096)."""
+    prior, chunk = 66000, 100
+    H.say(f"[case] append long prior {prior} chunk {chunk}")
+    b = wl.custom_batch([prior + chunk, 40], q_lens=[chunk, 1], num_q_heads=4, num_kv_heads=1,
+                        seed=77)
+    o, lse, cache, _ = H.run(b)
+    ro, rl, _, _ = _append_oracle(b)
+    H.assert_parity(o, lse, ro, rl, label="append long prior")
+    cache.close()
