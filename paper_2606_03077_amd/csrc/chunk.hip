@@ -4,9 +4,10 @@
 // [q0, q1)).  Query rows are (token, head) pairs of the G heads sharing KV head g, packed
 // into 16-wide matrix columns, tpb = max(1, 16 / G) tokens per column block; each wave
 // owns 2 column blocks, so a workgroup covers up to 16 * tpb tokens.  Keys are visited
-// 64 at a time: the step's eight 4 KiB tiles (K and V of 4 pages) are staged in LDS,
-// double-buffered, and shared by the 8 waves; V is interleaved by page pair on the way
-// in so that each PV operand is a single 16-byte LDS read.  Per page and column block:
+// 64 at a time: the step's eight 4 KiB tiles (K and V of 4 pages) are staged in LDS
+// (three stages) and shared by the 8 waves; V is interleaved by page pair on the way
+// in so that each PV operand is a single 16-byte LDS read.  Each wave computes the
+// next step's scores while it turns the current step's into probabilities.  Per page and column block:
 //   S^T = K . Q^T (4 mfma 16x16x32), and per page pair O^T += V^T . P^T (8 mfma 16x16x32
 //   over 32 keys).
 // Softmax runs online in base 2.  The running maximum is only moved (and the
@@ -18,6 +19,7 @@
 // Units arrive in per-XCD queues: workgroup w takes tile w / 8 of queue w % 8, so the
 // tiles of one (b, g), which read the same keys, run on one XCD and share its L2.
 #include <cmath>
+#include <type_traits>
 
 #include "internal.h"
 
@@ -33,15 +35,18 @@ constexpr int kNB = 2;           // column blocks per wave
 constexpr int kStepPages = 4;    // pages (16 keys each) per softmax step
 constexpr float kTau = 8.f;      // lazy-rescale threshold, base-2 logits
 constexpr int kMaxIds = 4096;    // block-table entries staged in LDS (64K keys)
+constexpr int kBufs = 3;         // LDS stages: step n (V), step n + 1 (K), step n + 2 (landing)
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 x) { return __builtin_bit_cast(bf16x8, x); }
 
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+// Two floats to bf16 (round to nearest even) in one v_cvt_pk_bf16_f32.
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  const __bf16 a = static_cast<__bf16>(lo);
-  const __bf16 b = static_cast<__bf16>(hi);
-  return uint32_t(__builtin_bit_cast(uint16_t, a)) | (uint32_t(__builtin_bit_cast(uint16_t, b)) << 16);
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2));
 }
 
 struct ChunkArgs {
@@ -66,8 +71,8 @@ void chunk_kernel(ChunkArgs A) {
   // V: [buffer][page pair][t][half][lane] x {page 2h bytes, page 2h+1 bytes}: for channel
   // block db = 2 t + half, lane l's 16 bytes are exactly its PV A operand (4 slots of
   // each page of the pair), so the PV loop reads operands with one ds_read_b128.
-  __shared__ uint4 ldk[2][kStepPages][256];
-  __shared__ uint2 ldv[2][kStepPages / 2][4][2][64][2];
+  __shared__ uint4 ldk[kBufs][kStepPages][256];
+  __shared__ uint2 ldv[kBufs][kStepPages / 2][4][2][64][2];
   __shared__ __align__(16) int lds_ids[kMaxIds];  // the tile's block-table row
 
   const int xcd = blockIdx.x % kNumXcds;
@@ -166,24 +171,8 @@ void chunk_kernel(ChunkArgs A) {
   for (int i = tid; i < nids; i += kThreads) lds_ids[i] = btrow[min(i, npages - 1)];
   __syncthreads();
 
-  uint4 stage[kStepPages];
-  if (nsteps > 0) {
-    fetch(0, stage);
-    stash(0, stage);
-  }
-  // Every load issued so far (Q operands, the first stage) has landed: the loop's
-  // wait counts then only track the in-loop prefetch.
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-
-  for (int n = 0; n < nsteps; ++n) {
-    const int buf = n & 1;
-    if (n + 1 < nsteps) fetch(n + 1, stage);
-    const int key0 = n * kStepPages * kPage;
-    const bool masked = key0 + kStepPages * kPage - 1 > first_tok || key0 + kStepPages * kPage > kv1;
-
-    // Scores of the step's 4 pages for both column blocks.
-    f32x4 s[kStepPages][kNB];
+  // Scores S^T = K . Q^T of one step's 4 pages for both column blocks.
+  auto qk = [&](int buf, f32x4 (&s)[kStepPages][kNB]) {
 #pragma unroll
     for (int j = 0; j < kStepPages; ++j) {
       uint4 kr[4];
@@ -197,17 +186,23 @@ void chunk_kernel(ChunkArgs A) {
         s[j][nb] = a;
       }
     }
+  };
 
-    bf16x8 pop[kNB][2];
+  // Step n's causal mask and running-maximum update (small, with branches): gives the
+  // exponent offset -m of each column block.
+  auto prepare = [&](int key0, f32x4 (&s)[kStepPages][kNB], float (&neg_m)[kNB]) {
+    const bool masked = key0 + kStepPages * kPage - 1 > first_tok || key0 + kStepPages * kPage > kv1;
+    if (masked) {
 #pragma unroll
-    for (int nb = 0; nb < kNB; ++nb) {
-      if (masked) {
+      for (int nb = 0; nb < kNB; ++nb)
 #pragma unroll
         for (int j = 0; j < kStepPages; ++j)
 #pragma unroll
           for (int r = 0; r < 4; ++r)
             if (key0 + j * kPage + 4 * quad + r > lim[nb]) s[j][nb][r] = -INFINITY;
-      }
+    }
+#pragma unroll
+    for (int nb = 0; nb < kNB; ++nb) {
       float mloc = -INFINITY;
 #pragma unroll
       for (int j = 0; j < kStepPages; ++j)
@@ -224,14 +219,24 @@ void chunk_kernel(ChunkArgs A) {
         for (int db = 0; db < 8; ++db) acc[nb][db] *= alpha;
         m[nb] = mc;
       }
-      const float neg_m = m[nb] == -INFINITY ? 0.f : -m[nb];
+      neg_m[nb] = m[nb] == -INFINITY ? 0.f : -m[nb];
+    }
+  };
+
+  // Branch-free: step n's probabilities (exp2, row sums, bf16 packing) interleaved with
+  // step n + 1's score MFMAs, which do not depend on them.
+  auto exp_and_next_qk = [&](int nbuf, const f32x4 (&s)[kStepPages][kNB],
+                             const float (&neg_m)[kNB], bf16x8 (&pop)[kNB][2],
+                             f32x4 (&s_next)[kStepPages][kNB]) {
+#pragma unroll
+    for (int nb = 0; nb < kNB; ++nb) {
       float p[kStepPages][4];
       float ps = 0.f;
 #pragma unroll
       for (int j = 0; j < kStepPages; ++j)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          p[j][r] = __builtin_amdgcn_exp2f(fmaf(s[j][nb][r], A.sl2, neg_m));
+          p[j][r] = __builtin_amdgcn_exp2f(fmaf(s[j][nb][r], A.sl2, neg_m[nb]));
           ps += p[j][r];
         }
       l[nb] += ps;
@@ -245,38 +250,97 @@ void chunk_kernel(ChunkArgs A) {
         pop[nb][h] = as_bf16x8(pb);
       }
     }
+    qk(nbuf, s_next);
+    // 16 K-operand reads first, then each score MFMA paired with an exponential and two
+    // other vector operations.
+    __builtin_amdgcn_sched_group_barrier(0x100, 16, 0);
+#pragma unroll
+    for (int i = 0; i < 32; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x400, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
+    }
+  };
 
-    // O^T += V^T P^T over each page pair (32 keys).
+  // O^T += V^T P^T over each page pair (32 keys) of one step.  On the last step, V of
+  // slots at or past kv1 (never written, possibly NaN) is zeroed in the operands.
+  auto pv = [&](int buf, int key0, const bf16x8 (&pop)[kNB][2], auto last_tag) {
+    constexpr bool kLast = decltype(last_tag)::value;
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-      // Slots at or past kv1 may hold NaN: zero them in the operands of the last pages.
-      const bool tail = key0 + (2 * h + 2) * kPage > kv1;
-      uint32_t ma0 = ~0u, ma1 = ~0u, mb0 = ~0u, mb1 = ~0u;
-      if (tail) {
+      uint4 vo[8];
+#pragma unroll
+      for (int db = 0; db < 8; ++db)
+        vo[db] = *reinterpret_cast<const uint4*>(&ldv[buf][h][db >> 1][db & 1][lane][0]);
+      if constexpr (kLast) {
         const int ka = min(max(kv1 - key0 - 2 * h * kPage - 4 * quad, 0), 4);
         const int kb = min(max(kv1 - key0 - (2 * h + 1) * kPage - 4 * quad, 0), 4);
-        ma0 = ka >= 2 ? ~0u : (ka == 1 ? 0x0000FFFFu : 0u);
-        ma1 = ka >= 4 ? ~0u : (ka == 3 ? 0x0000FFFFu : 0u);
-        mb0 = kb >= 2 ? ~0u : (kb == 1 ? 0x0000FFFFu : 0u);
-        mb1 = kb >= 4 ? ~0u : (kb == 3 ? 0x0000FFFFu : 0u);
+        const uint32_t ma0 = ka >= 2 ? ~0u : (ka == 1 ? 0x0000FFFFu : 0u);
+        const uint32_t ma1 = ka >= 4 ? ~0u : (ka == 3 ? 0x0000FFFFu : 0u);
+        const uint32_t mb0 = kb >= 2 ? ~0u : (kb == 1 ? 0x0000FFFFu : 0u);
+        const uint32_t mb1 = kb >= 4 ? ~0u : (kb == 3 ? 0x0000FFFFu : 0u);
+#pragma unroll
+        for (int db = 0; db < 8; ++db) {
+          vo[db].x &= ma0;
+          vo[db].y &= ma1;
+          vo[db].z &= mb0;
+          vo[db].w &= mb1;
+        }
       }
 #pragma unroll
-      for (int db = 0; db < 8; ++db) {
-        uint4 vo = *reinterpret_cast<const uint4*>(&ldv[buf][h][db >> 1][db & 1][lane][0]);
-        if (tail) {
-          vo.x &= ma0;
-          vo.y &= ma1;
-          vo.z &= mb0;
-          vo.w &= mb1;
-        }
+      for (int db = 0; db < 8; ++db)
 #pragma unroll
         for (int nb = 0; nb < kNB; ++nb)
-          acc[nb][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(vo), pop[nb][h], acc[nb][db], 0, 0, 0);
-      }
+          acc[nb][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(vo[db]), pop[nb][h], acc[nb][db], 0, 0, 0);
     }
+  };
 
-    if (n + 1 < nsteps) stash(buf ^ 1, stage);
+  // Software pipeline over steps, three LDS stages: while step n's probabilities are
+  // formed and multiplied into V, step n + 1's scores are computed from its K (the two
+  // are independent, so matrix and vector work interleave within each wave) and step
+  // n + 2 is in flight from memory.
+  uint4 stage[kStepPages];
+  if (nsteps > 0) {
+    fetch(0, stage);
+    stash(0, stage);
+  }
+  if (nsteps > 1) {
+    fetch(1, stage);
+    stash(1, stage);
+  }
+  // Every load issued so far (Q operands, the first stages) has landed: the loop's
+  // wait counts then only track the in-loop prefetch.
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+
+  f32x4 s_cur[kStepPages][kNB], s_nxt[kStepPages][kNB];
+  if (nsteps > 0) qk(0, s_cur);
+  // Steps before the last: no V tail to clear, so exp, next scores and PV form one
+  // branch-free block the scheduler can interleave.
+  for (int n = 0; n + 1 < nsteps; ++n) {
+    const int key0 = n * kStepPages * kPage;
+    if (n + 2 < nsteps) fetch(n + 2, stage);
+    float neg_m[kNB];
+    prepare(key0, s_cur, neg_m);
+    bf16x8 pop[kNB][2];
+    exp_and_next_qk((n + 1) % kBufs, s_cur, neg_m, pop, s_nxt);
+    pv(n % kBufs, key0, pop, std::false_type{});
+    if (n + 2 < nsteps) stash((n + 2) % kBufs, stage);
     __syncthreads();
+#pragma unroll
+    for (int j = 0; j < kStepPages; ++j)
+#pragma unroll
+      for (int nb = 0; nb < kNB; ++nb) s_cur[j][nb] = s_nxt[j][nb];
+  }
+  if (nsteps > 0) {
+    const int n = nsteps - 1;
+    const int key0 = n * kStepPages * kPage;
+    float neg_m[kNB];
+    prepare(key0, s_cur, neg_m);
+    bf16x8 pop[kNB][2];
+    // The next-score MFMAs read a stale stage here; their result is unused.
+    exp_and_next_qk((n + 1) % kBufs, s_cur, neg_m, pop, s_nxt);
+    pv(n % kBufs, key0, pop, std::true_type{});
   }
 
   // Epilogue: every column is owned by one wave; normalise and store.
