@@ -28,7 +28,10 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kWaves = 4;
+#ifndef LIBRA_DECODE_WAVES
+#define LIBRA_DECODE_WAVES 4
+#endif
+constexpr int kWaves = LIBRA_DECODE_WAVES;
 constexpr int kThreads = 64 * kWaves;
 #ifndef LIBRA_DECODE_DEPTH
 #define LIBRA_DECODE_DEPTH 2
@@ -264,7 +267,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(LIBRA_
   }
   __syncthreads();
 
-  // Each thread finishes 8 channels of one column (head).
+  // The first 256 threads each finish 8 channels of one column (head).
+  if (tid >= 256) return;
   const int hcol = tid >> 4, c8 = (tid & 15) * 8;
   float Mh = red_m[0][hcol];
 #pragma unroll
@@ -382,7 +386,7 @@ struct MergeArgs {
 // lse = M + log2(sum_j 2^(lse_j - M)), o = sum_j 2^(lse_j - lse) o_j; empty splits
 // (lse_j = -inf) add nothing.  Splits are read 8 at a time (all loads of a batch in
 // flight together) and folded in with a running maximum.
-__global__ __launch_bounds__(kThreads) void merge_kernel(MergeArgs A) {
+__global__ __launch_bounds__(256) void merge_kernel(MergeArgs A) {
   constexpr int kBatch = 8;
   const int32_t* m = A.merges + size_t(blockIdx.x) * kMergeInts;
   const int g = m[M_G], n = m[M_N], part = m[M_PART], row = m[M_ROW];
@@ -485,7 +489,7 @@ hipError_t launch_merge(const Plan& P, void* ws, void* out, float* lse, hipStrea
   A.lse = lse;
   A.hq = P.num_q_heads;
   A.group = P.group;
-  hipLaunchKernelGGL(merge_kernel, dim3(unsigned(n)), dim3(kThreads), 0, s, A);
+  hipLaunchKernelGGL(merge_kernel, dim3(unsigned(n)), dim3(256), 0, s, A);
   return hipGetLastError();
 }
 
