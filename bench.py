@@ -133,7 +133,7 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="7b",
-                    choices=["tiny", "7b", "longtail", "straggler", "append"])
+                    choices=["tiny", "7b", "longtail", "straggler", "append", "prefill"])
     ap.add_argument("--flush-mib", type=int, default=1024)
     ap.add_argument("--units-per-cu", type=int, default=4)
     ap.add_argument("--min-split-pages", type=int, default=16)

@@ -22,7 +22,7 @@ own device layout with its pack entry point):
 
 Recipe (fixed, so that every stored number can be regenerated):
 
-* seed = 26060 + config index (1..5), numpy PCG64 (``numpy.random.default_rng``);
+* seed = 26060 + config index (1..6), numpy PCG64 (``numpy.random.default_rng``);
 * draw order: lengths, chunk lengths, mixture positions, page permutation, q, K, V,
   k_new, v_new;
 * value draws: standard normal in float32, rounded to bf16 with round-to-nearest-even;
@@ -85,6 +85,12 @@ WORKLOADS = {
                        "append, B=128, Hq=32, Hkv=8, prior lognormal(median 4096, "
                        "sigma 1) clipped to [256,32768]; 25% append U[64,1024] tokens, "
                        "75% append 1 token", append=True),
+    # Recompute of a migrated request's KV on its target bucket: a full-context prefill
+    # (empty prior) at the paper's 40,960-token maximum model length, with the 40 query /
+    # 8 KV heads of its 14B policy (Sec. 5, cross-node migration; Sec. 7, Setup).
+    "prefill": Workload("prefill", 6, 1, 40, 8,
+                        "recompute prefill, B=1, Hq=40, Hkv=8, prior 0, 40960 new tokens",
+                        append=True),
 }
 
 
@@ -192,6 +198,8 @@ def draw_lengths(w: Workload, rng: np.random.Generator):
         return lens, np.ones(B, np.int64)
     if w.name == "straggler":
         return _uniform_int(rng, 98304, 131072, B), np.ones(B, np.int64)
+    if w.name == "prefill":
+        return np.full(B, 40960, np.int64), np.full(B, 40960, np.int64)
     if w.name == "append":
         prior = _lognormal_len(rng, 4096, 1.0, 256, 32768, B)
         n_chunk = B // 4

@@ -151,7 +151,7 @@ def test_decode_longtail_full_config_sampled():
     assert np.isfinite(o).all() and np.isfinite(lse).all()
 
 
-@pytest.mark.parametrize("hq,hkv", [(32, 8), (28, 4), (8, 8), (16, 1)])
+@pytest.mark.parametrize("hq,hkv", [(32, 8), (28, 4), (8, 8), (16, 1), (40, 8)])
 def test_append_mixed_chunks(hq, hkv):
     prior = [0, 7, 100, 1000, 33, 16, 5000, 250]
     chunk = [5, 1, 64, 300, 1, 16, 129, 1]
@@ -236,3 +236,36 @@ def test_append_prior_longer_than_staged_block_table():
     ro, rl, _, _ = _append_oracle(b)
     H.assert_parity(o, lse, ro, rl, label="append long prior")
     cache.close()
+
+
+@pytest.mark.parametrize("chunk", [1, 600, 2000])
+def test_recompute_prefill_empty_prior(chunk):
+    """Recompute of a migrated request's KV: an append with no prior context."""
+    H.say(f"[case] prefill P=0 C={chunk}")
+    b = wl.custom_batch([chunk], q_lens=[chunk], num_q_heads=40, num_kv_heads=8, seed=chunk,
+                        append=True)
+    o, lse, cache, _ = H.run(b)
+    ro, rl, k_after, v_after = _append_oracle(b)
+    H.assert_parity(o, lse, ro, rl, label=f"prefill C={chunk}")
+    k2, v2 = cache.unpack()
+    assert np.array_equal(k2, k_after) and np.array_equal(v2, v_after)
+    cache.close()
+
+
+def test_recompute_prefill_full_length_sampled():
+    """The 40,960-token recompute at full size; the oracle checks sampled query rows."""
+    H.say("[case] prefill 40960 full size")
+    b = wl.make_batch("prefill")
+    o, lse, cache, _ = H.run(b)
+    cache.close()
+    k_all = b.k_new  # prior is empty: the new tokens are the whole context
+    v_all = b.v_new
+    rows = [0, 1, 47, 48, 4095, 20000, 40959]
+    from oracle.attention import attend, bf16_bits_to_f64
+    G = 5
+    for r in rows:
+        for h in (0, 7, 21, 39):
+            g = h // G
+            ro, rl = attend(bf16_bits_to_f64(b.q[r, h])[None], bf16_bits_to_f64(k_all[:r + 1, g]),
+                            bf16_bits_to_f64(v_all[:r + 1, g]), b.scale)
+            H.assert_parity(o[r, h][None], lse[r, h][None], ro, rl, label=f"prefill row {r} head {h}")
