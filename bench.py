@@ -127,13 +127,206 @@ def cpu_baseline(batch, min_seconds: float = 10.0) -> dict:
             "decode_tokens_per_s": B * passes / el}
 
 
+PCIE_GEN5_X16_GBS = 64.0   # per direction, before protocol overhead
+
+
+def bench_migrate(args, torch, libra, wl) -> dict:
+    """Migration of one paused request between TP degrees (Sec. 5, Steps 1-3), per layer.
+
+    The request holds ``--migrate-tokens`` tokens of a 40-query-head / 8-KV-head model
+    (one layer's K and V).  Step 1: page gather into a packed device run, then a copy to
+    pinned host memory.  Step 2: host reshard from TP_src to TP_dst head shards.  Step 3:
+    each target shard's run is copied to the device and scattered into fresh pages (all
+    target caches live on this one GPU).  Device phases are timed with HIP events on
+    one stream, the host reshard with the wall clock.
+    """
+    tp_src, tp_dst = (int(x) for x in args.migrate_tp.split(","))
+    hq, hkv, L = 40, 8, args.migrate_tokens
+    if hkv % tp_src or hkv % tp_dst:
+        raise SystemExit("TP degrees must divide the 8 KV heads")
+    n = -(-L // 16)
+    tile = 2048
+    log(f"[bench] migrate: {L} tokens, TP {tp_src} -> {tp_dst}")
+    batch = wl.custom_batch([L], num_q_heads=hq, num_kv_heads=hkv, seed=L, poison=False)
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    # TP_src source caches, each holding its head range of the request's pages
+    full_k = batch.k_pages
+    full_v = batch.v_pages
+    P = full_k.shape[0]
+    hs = hkv // tp_src
+    src = []
+    for i in range(tp_src):
+        k = torch.empty(P * hs * tile, dtype=torch.int16, device=dev)
+        v = torch.empty_like(k)
+        lay = libra.libra_kv_layout_create(k, v, P, hs)
+        kl = torch.from_numpy(np.ascontiguousarray(full_k[:, i * hs:(i + 1) * hs]).view(np.int16))
+        vl = torch.from_numpy(np.ascontiguousarray(full_v[:, i * hs:(i + 1) * hs]).view(np.int16))
+        libra.libra_kv_pack_pages(lay, kl.to(dev), vl.to(dev), 0, P)
+        src.append((lay, k, v))
+    ids = torch.from_numpy(np.ascontiguousarray(batch.block_table[0, :n])).to(dev)
+    hd = hkv // tp_dst
+    rng = np.random.default_rng(7)
+    dst = []
+    for j in range(tp_dst):
+        k = torch.empty((n + 64) * hd * tile, dtype=torch.int16, device=dev)
+        v = torch.empty_like(k)
+        lay = libra.libra_kv_layout_create(k, v, n + 64, hd)
+        tid = torch.from_numpy(rng.permutation(n + 64)[:n].astype(np.int32)).to(dev)
+        dst.append((lay, k, v, tid))
+    run_k = [torch.empty(n * hs * tile, dtype=torch.int16, device=dev) for _ in range(tp_src)]
+    run_v = [torch.empty_like(r) for r in run_k]
+    host_k = [torch.empty(r.shape, dtype=torch.int16, pin_memory=True) for r in run_k]
+    host_v = [torch.empty(r.shape, dtype=torch.int16, pin_memory=True) for r in run_k]
+    out_k = [torch.empty(n * hd * tile, dtype=torch.int16, pin_memory=True) for _ in range(tp_dst)]
+    out_v = [torch.empty(r.shape, dtype=torch.int16, pin_memory=True) for r in out_k]
+    dev_k = [torch.empty(r.shape, dtype=torch.int16, device=dev) for r in out_k]
+    dev_v = [torch.empty_like(r) for r in dev_k]
+    torch.cuda.synchronize()
+
+    def ev():
+        return torch.cuda.Event(enable_timing=True)
+
+    phases = {"copy_out_kernel": [], "d2h": [], "reshard_host": [], "h2d": [],
+              "copy_in_kernel": []}
+    iters = max(1, args.steps)
+    for it in range(args.warmup + iters):
+        e = [ev() for _ in range(6)]
+        e[0].record(stream)
+        for i, (lay, _, _) in enumerate(src):
+            libra.libra_kv_copy_out(lay, ids, n, run_k[i], run_v[i], stream=stream)
+        e[1].record(stream)
+        for i in range(tp_src):
+            host_k[i].copy_(run_k[i], non_blocking=True)
+            host_v[i].copy_(run_v[i], non_blocking=True)
+        e[2].record(stream)
+        stream.synchronize()
+        t0 = time.perf_counter()
+        libra.libra_kv_reshard_host(host_k, hs, out_k, n)
+        libra.libra_kv_reshard_host(host_v, hs, out_v, n)
+        t_reshard = (time.perf_counter() - t0) * 1e3
+        e[3].record(stream)
+        for j in range(tp_dst):
+            dev_k[j].copy_(out_k[j], non_blocking=True)
+            dev_v[j].copy_(out_v[j], non_blocking=True)
+        e[4].record(stream)
+        for j, (lay, _, _, tid) in enumerate(dst):
+            libra.libra_kv_copy_in(lay, tid, n, dev_k[j], dev_v[j], stream=stream)
+        e[5].record(stream)
+        stream.synchronize()
+        if it >= args.warmup:
+            phases["copy_out_kernel"].append(e[0].elapsed_time(e[1]))
+            phases["d2h"].append(e[1].elapsed_time(e[2]))
+            phases["reshard_host"].append(t_reshard)
+            phases["h2d"].append(e[3].elapsed_time(e[4]))
+            phases["copy_in_kernel"].append(e[4].elapsed_time(e[5]))
+        log(f"[bench] migrate iteration {it} done")
+
+    def check_targets(what):
+        """The target pages hold exactly the resharded runs (bit-exact)."""
+        for j, (lay, _, _, tid) in enumerate(dst):
+            kk = torch.empty(n * hd * tile, dtype=torch.int16, device=dev)
+            vv = torch.empty_like(kk)
+            libra.libra_kv_copy_out(lay, tid, n, kk, vv, stream=stream)
+            stream.synchronize()
+            if not (torch.equal(kk.cpu(), out_k[j]) and torch.equal(vv.cpu(), out_v[j])):
+                raise RuntimeError(f"{what}: migrated pages differ from the resharded run")
+
+    check_targets("staged")
+    for lay, k, v, tid in dst:
+        k.fill_(0)
+        v.fill_(0)
+    # Direct variant: the copy kernels read / write the pinned host runs themselves, so
+    # each of offload and reload is one kernel crossing PCIe (no device staging buffer).
+    direct = {"copy_out_direct": [], "copy_in_direct": []}
+    for it in range(args.warmup + iters):
+        e = [ev() for _ in range(4)]
+        e[0].record(stream)
+        for i, (lay, _, _) in enumerate(src):
+            libra.libra_kv_copy_out(lay, ids, n, host_k[i], host_v[i], stream=stream)
+        e[1].record(stream)
+        stream.synchronize()
+        libra.libra_kv_reshard_host(host_k, hs, out_k, n)
+        libra.libra_kv_reshard_host(host_v, hs, out_v, n)
+        e[2].record(stream)
+        for j, (lay, _, _, tid) in enumerate(dst):
+            libra.libra_kv_copy_in(lay, tid, n, out_k[j], out_v[j], stream=stream)
+        e[3].record(stream)
+        stream.synchronize()
+        if it >= args.warmup:
+            direct["copy_out_direct"].append(e[0].elapsed_time(e[1]))
+            direct["copy_in_direct"].append(e[2].elapsed_time(e[3]))
+    log("[bench] migrate direct variant done")
+    check_targets("direct")
+    med = {k: float(np.median(v)) for k, v in phases.items()}
+    med_direct = {k: float(np.median(v)) for k, v in direct.items()}
+    layer_bytes = n * hkv * tile * 2 * 2          # K and V of one layer, whole pages
+    gbs = lambda ms, b: b / (ms * 1e-3) / 1e9
+    offload_ms = med["copy_out_kernel"] + med["d2h"]
+    reload_ms = med["h2d"] + med["copy_in_kernel"]
+    total_ms = offload_ms + med["reshard_host"] + reload_ms
+    copy_kernel_gbs = gbs(med["copy_out_kernel"], 2 * layer_bytes)
+    for lay, _, _ in src:
+        libra.libra_kv_layout_destroy(lay)
+    for lay, _, _, _ in dst:
+        libra.libra_kv_layout_destroy(lay)
+    result = {
+        "metric": "KV migration latency per layer (offload + head reshard + reload)",
+        "value": round(total_ms, 4),
+        "unit": "ms/layer",
+        "n_gpus": 1, "steps": iters, "warmup": args.warmup,
+        "ms_per_step": round(total_ms, 4),
+        "higher_is_better": False, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic (seeded normal bf16 pages)",
+        "config": {"workload": f"migrate: one {L}-token request, 40 query / 8 KV heads, "
+                               f"head_dim 128, TP {tp_src} -> {tp_dst}, one layer",
+                   "pages": n, "layer_kv_bytes": layer_bytes},
+        "phases_ms_median": {k: round(v, 4) for k, v in med.items()},
+        "direct_ms_median": {k: round(v, 4) for k, v in med_direct.items()},
+        "direct_GBps": {k: round(gbs(v, layer_bytes), 2) for k, v in med_direct.items()},
+        "offload_ms": round(offload_ms, 4),
+        "reload_ms": round(reload_ms, 4),
+        "d2h_GBps": round(gbs(med["d2h"], layer_bytes), 2),
+        "h2d_GBps": round(gbs(med["h2d"], layer_bytes), 2),
+        "reshard_host_GBps": round(gbs(med["reshard_host"], layer_bytes), 2),
+        "pcie_peak_GBps_per_direction": PCIE_GEN5_X16_GBS,
+        "roofline": {"bound": "hbm", "achieved": round(copy_kernel_gbs, 2), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(copy_kernel_gbs / HBM_PEAK_GBS, 4),
+                     "traffic": None, "kernel": "page_copy_kernel (copy_out)",
+                     "algorithmic_bytes_per_launch": 2 * layer_bytes // tp_src,
+                     "kernel_avg_ms": round(med["copy_out_kernel"] / tp_src, 5)},
+    }
+    if not args.no_cpu_baseline:
+        import oracle.migration as om
+        req_k = om.request_pages(batch.k_pages, batch.block_table[0], L)
+        req_v = om.request_pages(batch.v_pages, batch.block_table[0], L)
+        srcs_k = om.reshard_heads([req_k], tp_src)
+        srcs_v = om.reshard_heads([req_v], tp_src)
+        reps, t0 = 0, time.perf_counter()
+        while time.perf_counter() - t0 < min(args.cpu_seconds, 5.0):
+            om.reshard_heads(srcs_k, tp_dst)
+            om.reshard_heads(srcs_v, tp_dst)
+            reps += 1
+        el = time.perf_counter() - t0
+        result["cpu_baseline"] = {
+            "value": round(layer_bytes * reps / el / 1e9, 3), "unit": "GB/s", "cores": 1,
+            "kind": "oracle",
+            "sample": f"numpy head reshard of the request's pages (one layer) x {reps}, {el:.1f} s"}
+    return result
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="7b",
-                    choices=["tiny", "7b", "longtail", "straggler", "append", "prefill"])
+                    choices=["tiny", "7b", "longtail", "straggler", "append", "prefill",
+                             "migrate"])
+    ap.add_argument("--migrate-tokens", type=int, default=40960,
+                    help="migrate workload: prefix length of the migrated request")
+    ap.add_argument("--migrate-tp", default="1,2",
+                    help="migrate workload: source and target TP degree (head shards)")
     ap.add_argument("--flush-mib", type=int, default=1024)
     ap.add_argument("--units-per-cu", type=int, default=4)
     ap.add_argument("--min-split-pages", type=int, default=16)
@@ -171,6 +364,9 @@ def main():
         raise RuntimeError(f"expected one HIP runtime, found {libra.hip_runtimes_mapped()}")
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.workload == "migrate":
+        print(json.dumps(bench_migrate(args, torch, libra, wl)), flush=True)
+        return
 
     log(f"[bench] generating workload {args.workload}")
     t = time.perf_counter()

@@ -124,6 +124,46 @@ libra_status libra_kv_gather(libra_kv_layout layout, const int32_t* block_table,
                              void* k_out, void* v_out, void* stream);
 
 /* ------------------------------------------------------------------------------ */
+/* Request migration: offload, head reshard, reload                                */
+/* ------------------------------------------------------------------------------ */
+/*
+ * When a request pauses for a tool call, its KV pages are offloaded to host pinned
+ * memory; while the tool runs they are resharded along the attention-head axis to the
+ * target bucket's tensor-parallel degree; when the tool returns, each target GPU
+ * reloads its head shard into pages of its own cache (Sec. 5, migration Steps 1-3).
+ * Pages move as raw library-layout tiles, so no step re-encodes data.
+ *
+ * A page's tiles for all KV heads are contiguous: page p of K occupies bytes
+ * [p * Hkv * 4096, (p + 1) * Hkv * 4096) of k_cache (likewise V).  A packed page run is
+ * n_pages such blocks back to back.
+ */
+
+/* Gathers pages page_ids[0 .. n_pages) (device int32, n_pages <= num_pages) of the cache
+ * into packed runs k_dst / v_dst of n_pages * Hkv * 4096 bytes each (either may be NULL).
+ * A run is device memory, or pinned host memory (hipHostMalloc): then the kernel writes
+ * it over PCIe itself, which offloads a request in one call.  Pageable host memory is
+ * refused (LIBRA_E_INVAL).  Ids outside [0, num_pages) are skipped and leave their run
+ * block unchanged.  Asynchronous on `stream`; the caller owns every buffer. */
+libra_status libra_kv_copy_out(libra_kv_layout layout, const int32_t* page_ids, int64_t n_pages,
+                               void* k_dst, void* v_dst, void* stream);
+
+/* Scatters packed runs k_src / v_src (device or pinned host memory, as above; either may
+ * be NULL) into pages page_ids[0 .. n_pages) of the cache: the reload of a request.  The
+ * ids must be distinct (repeated ids race); ids outside [0, num_pages) are skipped. */
+libra_status libra_kv_copy_in(libra_kv_layout layout, const int32_t* page_ids, int64_t n_pages,
+                              const void* k_src, const void* v_src, void* stream);
+
+/* Host-side reshard of packed page runs along the head axis (pure memory
+ * rearrangement, no device work).  The n_src inputs hold heads_per_src heads each, in
+ * head order (source shard i owns heads [i * heads_per_src, (i + 1) * heads_per_src));
+ * their H = n_src * heads_per_src heads are dealt to n_dst outputs of H / n_dst
+ * contiguous heads each.  A TP degree raised k-fold is (1 source, k outputs); lowered,
+ * (k sources, 1 output).  All buffers are host memory of n_pages * heads * 4096 bytes
+ * and must not overlap.  Returns LIBRA_E_INVAL if n_dst does not divide H. */
+libra_status libra_kv_reshard_host(const void* const* src, int32_t n_src, int32_t heads_per_src,
+                                   void* const* dst, int32_t n_dst, int64_t n_pages);
+
+/* ------------------------------------------------------------------------------ */
 /* Split-KV work plan (host)                                                       */
 /* ------------------------------------------------------------------------------ */
 /*
@@ -267,7 +307,9 @@ enum {
   LIBRA_KERNEL_MERGE = 5,
   LIBRA_KERNEL_CHUNK = 6,
   LIBRA_KERNEL_UPLOAD = 7,
-  LIBRA_KERNEL_KINDS = 8
+  LIBRA_KERNEL_COPY_OUT = 8,
+  LIBRA_KERNEL_COPY_IN = 9,
+  LIBRA_KERNEL_KINDS = 10
 };
 
 typedef struct libra_kernel_times {

@@ -34,3 +34,4 @@ from .attention import (  # noqa: F401
     merge_ref,
 )
 from .plan import plan_ref, PlanParams, UNIT_FIELDS  # noqa: F401
+from .migration import reshard_heads, request_pages, query_heads_of_shard  # noqa: F401

@@ -22,7 +22,7 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "liblibra.so")
 ARCH = "gfx950"
 
-SOURCES = ["api.cpp", "plan.cpp", "kv_layout.hip", "decode.hip", "chunk.hip"]
+SOURCES = ["api.cpp", "plan.cpp", "migrate.cpp", "kv_layout.hip", "decode.hip", "chunk.hip"]
 
 # Packed-fp32 VALU forms are disabled for all device code (the host pass warns that it
 # does not know the feature; that is harmless).
@@ -59,7 +59,7 @@ def build(verbose: bool = True) -> str:
     with cf.ThreadPoolExecutor(max_workers=min(8, len(SOURCES))) as ex:
         objs = list(ex.map(lambda s: _compile(s, save), SOURCES))
     tmp = LIB + ".tmp"
-    cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]
+    cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-pthread", *objs, "-o", tmp]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stderr}")

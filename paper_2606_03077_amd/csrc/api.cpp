@@ -203,6 +203,52 @@ libra_status launch_attention(const KvLayout& L, const Plan& P, void* ws, const 
   return e == hipSuccess ? LIBRA_OK : hip_error(e, "merge launch");
 }
 
+// The address a kernel uses for a page run: device memory as is, pinned host memory
+// through its device mapping (the copy then crosses PCIe inside the kernel).  Memory the
+// runtime does not know (pageable host memory) is refused.
+bool device_view(const void* p, void** out) {
+  hipPointerAttribute_t a{};
+  if (hipPointerGetAttributes(&a, p) != hipSuccess) {
+    (void)hipGetLastError();  // clear the runtime's last error; the caller reports its own
+    return false;
+  }
+  if (a.type == hipMemoryTypeDevice) {
+    *out = const_cast<void*>(p);
+    return true;
+  }
+  if (a.type == hipMemoryTypeHost && a.devicePointer && a.hostPointer) {
+    *out = static_cast<char*>(a.devicePointer) +
+           (static_cast<const char*>(p) - static_cast<const char*>(a.hostPointer));
+    return true;
+  }
+  return false;
+}
+
+libra_status page_copy(const KvLayout* layout, const int32_t* page_ids, int64_t n_pages,
+                       const void* k_run, const void* v_run, bool to_run, void* stream) {
+  if (!layout) return set_error(LIBRA_E_INVAL, "layout is NULL");
+  if (!k_run && !v_run) return set_error(LIBRA_E_INVAL, "K and V page runs are both NULL");
+  if (n_pages < 0 || n_pages > layout->desc.num_pages)
+    return set_error(LIBRA_E_INVAL, "n_pages must be in [0, num_pages]");
+  if (n_pages == 0) return LIBRA_OK;
+  if (!page_ids) return set_error(LIBRA_E_INVAL, "page_ids is NULL");
+  if ((k_run && !aligned16(k_run)) || (v_run && !aligned16(v_run)))
+    return set_error(LIBRA_E_INVAL, "page runs must be 16-byte aligned");
+  void* k_dev = nullptr;
+  void* v_dev = nullptr;
+  if (k_run && !device_view(k_run, &k_dev))
+    return set_error(LIBRA_E_INVAL, "K page run is neither device nor pinned host memory");
+  if (v_run && !device_view(v_run, &v_dev))
+    return set_error(LIBRA_E_INVAL, "V page run is neither device nor pinned host memory");
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e;
+  {
+    ProfScope ps(to_run ? LIBRA_KERNEL_COPY_OUT : LIBRA_KERNEL_COPY_IN, s, true);
+    e = launch_page_copy(*layout, page_ids, n_pages, k_dev, v_dev, to_run, s);
+  }
+  return e == hipSuccess ? LIBRA_OK : hip_error(e, "page copy launch");
+}
+
 }  // namespace
 }  // namespace libra
 
@@ -293,6 +339,16 @@ libra_status libra_kv_gather(libra_kv_layout layout, const int32_t* block_table,
                       static_cast<hipStream_t>(stream));
   }
   return e == hipSuccess ? LIBRA_OK : hip_error(e, "gather launch");
+}
+
+libra_status libra_kv_copy_out(libra_kv_layout layout, const int32_t* page_ids, int64_t n_pages,
+                               void* k_dst, void* v_dst, void* stream) {
+  return page_copy(layout, page_ids, n_pages, k_dst, v_dst, true, stream);
+}
+
+libra_status libra_kv_copy_in(libra_kv_layout layout, const int32_t* page_ids, int64_t n_pages,
+                              const void* k_src, const void* v_src, void* stream) {
+  return page_copy(layout, page_ids, n_pages, k_src, v_src, false, stream);
 }
 
 libra_status libra_splitkv_plan(const libra_plan_desc* desc, const int32_t* seq_lens_host,

@@ -83,6 +83,9 @@ hipError_t launch_cache_write(const KvLayout& L, const Plan& P, const void* ws, 
 hipError_t launch_decode(const KvLayout& L, const Plan& P, void* ws, const void* q,
                          const int32_t* bt, int32_t stride, float scale, void* out, float* lse,
                          hipStream_t s);
+// Page-run copies (to_run: cache -> packed run; else packed run -> cache).
+hipError_t launch_page_copy(const KvLayout& L, const int32_t* ids, int64_t n, void* k_run,
+                            void* v_run, bool to_run, hipStream_t s);
 hipError_t launch_zero_i32(int32_t* p, int64_t n, hipStream_t s);
 hipError_t launch_merge(const Plan& P, void* ws, void* out, float* lse, hipStream_t s);
 bool merge_launches(const Plan& P);  // whether launch_merge enqueues a kernel for P

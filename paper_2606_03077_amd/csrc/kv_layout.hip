@@ -6,6 +6,8 @@
 // kernels' 16-byte lane loads expect it (see k_off / v_off).  Every kernel stages one
 // tile per 256-thread block: thread t owns logical slot t / 16 and channels
 // 8 * (t % 16) .. + 7, and 16 contiguous bytes of the library-order tile at 16 t.
+#include <algorithm>
+
 #include "internal.h"
 
 namespace libra {
@@ -136,6 +138,36 @@ __global__ __launch_bounds__(kThreads) void cache_write_kernel(
   *reinterpret_cast<uint4*>(v_cache + base + t * 8) = *reinterpret_cast<const uint4*>(vt + t * 8);
 }
 
+// Moves whole (page, head) tiles between the cache and a packed page run (request
+// offload and reload): run tile r = i * hkv + g holds tile g of page ids[i].  A tile is
+// 256 lanes x 16 bytes, so each block-iteration moves one K and one V tile; blocks stride
+// over the run.  Ids outside [0, num_pages) are skipped.
+template <bool kToRun>
+__global__ __launch_bounds__(kThreads) void page_copy_kernel(uint4* __restrict__ k_cache,
+                                                             uint4* __restrict__ v_cache,
+                                                             const int32_t* __restrict__ ids,
+                                                             int64_t num_pages, int hkv,
+                                                             int64_t tiles,
+                                                             uint4* __restrict__ k_run,
+                                                             uint4* __restrict__ v_run) {
+  const int t = threadIdx.x;
+  for (int64_t r = blockIdx.x; r < tiles; r += gridDim.x) {
+    const int64_t i = r / hkv;
+    const int g = int(r - i * hkv);
+    const int64_t page = ids[i];
+    if (page < 0 || page >= num_pages) continue;  // uniform per block
+    const size_t c = (size_t(page) * hkv + g) * kThreads + t;
+    const size_t q = size_t(r) * kThreads + t;
+    if (kToRun) {
+      if (k_run) k_run[q] = k_cache[c];
+      if (v_run) v_run[q] = v_cache[c];
+    } else {
+      if (k_run) k_cache[c] = k_run[q];
+      if (v_run) v_cache[c] = v_run[q];
+    }
+  }
+}
+
 // Clears the split-merge counters (a kernel rather than a memset, so that the upload
 // can be captured in a HIP graph).
 __global__ void zero_i32_kernel(int32_t* p, int64_t n) {
@@ -199,6 +231,20 @@ hipError_t launch_cache_write(const KvLayout& L, const Plan& P, const void* ws, 
                      static_cast<uint16_t*>(L.desc.k_cache), static_cast<uint16_t*>(L.desc.v_cache),
                      writes, bt, stride, hkv, static_cast<const uint16_t*>(k_new),
                      static_cast<const uint16_t*>(v_new));
+  return hipGetLastError();
+}
+
+hipError_t launch_page_copy(const KvLayout& L, const int32_t* ids, int64_t n, void* k_run,
+                            void* v_run, bool to_run, hipStream_t s) {
+  const int hkv = L.desc.num_kv_heads;
+  const int64_t tiles = n * hkv;
+  if (tiles == 0) return hipSuccess;
+  const unsigned blocks = unsigned(std::min<int64_t>(tiles, 16384));
+  auto kern = to_run ? page_copy_kernel<true> : page_copy_kernel<false>;
+  hipLaunchKernelGGL(kern, dim3(blocks), dim3(kThreads), 0, s,
+                     static_cast<uint4*>(L.desc.k_cache), static_cast<uint4*>(L.desc.v_cache), ids,
+                     L.desc.num_pages, hkv, tiles, static_cast<uint4*>(k_run),
+                     static_cast<uint4*>(v_run));
   return hipGetLastError();
 }
 

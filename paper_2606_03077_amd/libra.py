@@ -30,11 +30,13 @@ UNIT_FIELDS = ("b", "g", "kv_begin", "kv_end", "q_begin", "q_end", "split", "n_s
 
 EXPORTS = ("libra_status_string", "libra_last_error", "libra_kv_layout_create",
            "libra_kv_layout_destroy", "libra_kv_pack_pages", "libra_kv_unpack_pages",
-           "libra_kv_gather", "libra_splitkv_plan", "libra_plan_get_units", "libra_plan_get_info",
+           "libra_kv_gather", "libra_kv_copy_out", "libra_kv_copy_in", "libra_kv_reshard_host",
+           "libra_splitkv_plan", "libra_plan_get_units", "libra_plan_get_info",
            "libra_plan_workspace_bytes", "libra_plan_upload", "libra_plan_destroy",
            "libra_decode_attn", "libra_append_attn", "libra_profile_enable",
            "libra_profile_collect")
-KERNEL_KINDS = ("pack", "unpack", "gather", "cache_write", "decode", "merge", "chunk", "upload")
+KERNEL_KINDS = ("pack", "unpack", "gather", "cache_write", "decode", "merge", "chunk", "upload",
+                "copy_out", "copy_in")
 
 
 class LibraError(RuntimeError):
@@ -100,6 +102,10 @@ def load() -> ctypes.CDLL:
         "libra_kv_pack_pages": (ctypes.c_int, [P, P, P, I64, I64, P]),
         "libra_kv_unpack_pages": (ctypes.c_int, [P, P, P, I64, I64, P]),
         "libra_kv_gather": (ctypes.c_int, [P, P, I32, P, I32, I32, P, P, P]),
+        "libra_kv_copy_out": (ctypes.c_int, [P, P, I64, P, P, P]),
+        "libra_kv_copy_in": (ctypes.c_int, [P, P, I64, P, P, P]),
+        "libra_kv_reshard_host": (ctypes.c_int, [ctypes.POINTER(P), I32, I32, ctypes.POINTER(P),
+                                                 I32, I64]),
         "libra_splitkv_plan": (ctypes.c_int, [ctypes.POINTER(PlanDesc), I32P, I32P,
                                               ctypes.POINTER(PlanParams), ctypes.POINTER(P)]),
         "libra_plan_get_units": (ctypes.c_int, [P, ctypes.POINTER(I32P), I32P]),
@@ -146,6 +152,32 @@ def _ptr(t) -> Optional[int]:
     return int(t)
 
 
+def _host_ptr(t) -> Optional[int]:
+    if t is None:
+        return None
+    if isinstance(t, torch.Tensor):
+        if t.device.type != "cpu":
+            raise ValueError("host tensor expected")
+        if not t.is_contiguous():
+            raise ValueError("contiguous tensor expected")
+        return t.data_ptr()
+    if isinstance(t, np.ndarray):
+        if not t.flags.c_contiguous:
+            raise ValueError("contiguous array expected")
+        return t.ctypes.data
+    return int(t)
+
+
+def _run_ptr(t) -> Optional[int]:
+    """A page run: a device tensor, or a host tensor / array (the library accepts pinned
+    host memory and refuses pageable memory)."""
+    if isinstance(t, torch.Tensor) and t.device.type == "cpu":
+        return _host_ptr(t)
+    if isinstance(t, np.ndarray):
+        return _host_ptr(t)
+    return _ptr(t)
+
+
 def _stream(stream) -> Optional[int]:
     if stream is None:
         return torch.cuda.current_stream().cuda_stream
@@ -188,6 +220,30 @@ def libra_kv_pack_pages(layout: int, k_src, v_src, first_page: int, n_pages: int
 def libra_kv_unpack_pages(layout: int, k_dst, v_dst, first_page: int, n_pages: int, stream=None):
     _check(load().libra_kv_unpack_pages(layout, _ptr(k_dst), _ptr(v_dst), first_page, n_pages,
                                         _stream(stream)), "libra_kv_unpack_pages")
+
+
+def libra_kv_copy_out(layout: int, page_ids, n_pages: int, k_dst, v_dst, stream=None):
+    """Gathers pages page_ids[:n_pages] (device int32) into packed runs k_dst / v_dst
+    (device memory, or pinned host memory written directly over PCIe)."""
+    _check(load().libra_kv_copy_out(layout, _ptr(page_ids), n_pages, _run_ptr(k_dst),
+                                    _run_ptr(v_dst), _stream(stream)), "libra_kv_copy_out")
+
+
+def libra_kv_copy_in(layout: int, page_ids, n_pages: int, k_src, v_src, stream=None):
+    """Scatters packed runs k_src / v_src (device or pinned host memory) into pages
+    page_ids[:n_pages] (distinct)."""
+    _check(load().libra_kv_copy_in(layout, _ptr(page_ids), n_pages, _run_ptr(k_src),
+                                   _run_ptr(v_src), _stream(stream)), "libra_kv_copy_in")
+
+
+def libra_kv_reshard_host(src: Sequence, heads_per_src: int, dst: Sequence, n_pages: int):
+    """Regroups host page runs along heads: len(src) shards of heads_per_src heads each
+    become len(dst) shards of equal contiguous head ranges."""
+    P = ctypes.c_void_p
+    sp = (P * len(src))(*[_host_ptr(x) for x in src])
+    dp = (P * len(dst))(*[_host_ptr(x) for x in dst])
+    _check(load().libra_kv_reshard_host(sp, len(src), heads_per_src, dp, len(dst), n_pages),
+           "libra_kv_reshard_host")
 
 
 def libra_kv_gather(layout: int, block_table, bt_stride: int, cu_seq_lens, batch: int,

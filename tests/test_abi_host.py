@@ -178,6 +178,15 @@ def test_call_validation_codes_before_any_launch():
     assert lib.libra_append_attn(lay, aplan, fake, None, fake, fake, 7, 2, 8, 0.1, fake * 4,
                                  1 << 20, fake * 8, None, None) == 1  # null k_new
     assert "k_new" in libra.libra_last_error()
+    # page-run copies (request offload / reload)
+    for fn in (lib.libra_kv_copy_out, lib.libra_kv_copy_in):
+        assert fn(None, fake, 4, fake * 16, None, None) == 1       # null layout
+        assert fn(lay, fake, 4, None, None, None) == 1             # no run at all
+        assert fn(lay, fake, -1, fake * 16, None, None) == 1       # negative count
+        assert fn(lay, fake, 65, fake * 16, fake * 32, None) == 1  # more than num_pages
+        assert fn(lay, None, 4, fake * 16, None, None) == 1        # null ids
+        assert fn(lay, fake, 4, fake * 16 + 8, None, None) == 1    # misaligned run
+        assert fn(lay, None, 0, fake * 16, None, None) == 0        # empty: nothing launched
     libra.libra_plan_destroy(plan)
     libra.libra_plan_destroy(aplan)
     lib.libra_kv_layout_destroy(lay)

@@ -96,3 +96,30 @@ def test_merge_sign_slip_is_caught(monkeypatch):
     import oracle
     monkeypatch.setattr(oracle, "merge_ref", wrong)
     assert _caught(pins.test_split_anywhere_then_merge_equals_unsplit, [7, 8, 300])
+
+
+# --- head reshard (Sec. 5, Step 2) --------------------------------------------------
+
+def _interleaved_heads(shards, n_dst):
+    full = np.concatenate([np.asarray(s) for s in shards], axis=1)
+    return [full[:, j::n_dst].copy() for j in range(n_dst)]
+
+
+def _reversed_targets(shards, n_dst):
+    import oracle.migration as om
+    return om.reshard_heads(shards, n_dst)[::-1]
+
+
+def _sources_joined_backwards(shards, n_dst):
+    import oracle.migration as om
+    return om.reshard_heads(list(shards)[::-1], n_dst)
+
+
+@pytest.mark.parametrize("mutant", [_interleaved_heads, _reversed_targets,
+                                    _sources_joined_backwards], ids=lambda f: f.__name__)
+def test_reshard_mutants_are_caught(monkeypatch, mutant):
+    import test_migration_oracle as mig
+    monkeypatch.setattr(mig, "reshard_heads", mutant)
+    caught = [_caught(mig.test_split_by_brute_force), _caught(mig.test_join_by_brute_force),
+              _caught(mig.test_shard_decode_reproduces_full_heads, 32, 8, 4)]
+    assert any(caught), caught
