@@ -315,6 +315,223 @@ def bench_migrate(args, torch, libra, wl) -> dict:
     return result
 
 
+CE_DECODE_LENS = [256, 512, 1024, 2048, 4096, 8192, 12288, 16384, 24576, 32768, 40960]
+CE_PREFILL_LENS = [1024, 2048, 4096, 8192, 12288, 16384, 24576, 32768, 40960]
+
+
+def bench_ce(args, torch, libra) -> dict:
+    """Cost-evaluator calibration from this library's own attention timings (Sec. 4.5;
+    App. B.1; Sec. 7.5).
+
+    Per layer of a 40-query / 8-KV-head model: (a) a decode step over 32 sequences all
+    at context L, (b) the recompute prefill of one L-token sequence (append with empty
+    prior).  Each is timed with HIP events (median of --steps, L2 / MALL flushed before
+    every call).  T(L) = gamma L^2 + eta L + theta is fitted to every other length and
+    scored by MAPE on the lengths left out, then refitted on all of them.
+    """
+    hq, hkv, B = 40, 8, 32
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(2606)
+
+    def randn_i16(n):
+        return torch.randn(n, generator=gen, device=dev, dtype=torch.bfloat16).view(torch.int16)
+
+    flush = torch.empty(args.flush_mib * (1 << 20) // 4, dtype=torch.float32, device=dev)
+    reps = max(3, args.steps)
+
+    def timed(call):
+        ts = []
+        for r in range(args.warmup + reps):
+            flush.fill_(float(r))
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            call()
+            b.record(stream)
+            stream.synchronize()
+            if r >= args.warmup:
+                ts.append(a.elapsed_time(b))
+        return float(np.median(ts))
+
+    rng = np.random.default_rng(2606)
+    max_pages = 40960 // 16
+    # (a) decode steps
+    P = B * max_pages + 1
+    log(f"[bench] ce: filling a {P}-page cache on the device")
+    k = randn_i16(P * hkv * 2048)
+    v = randn_i16(P * hkv * 2048)
+    layout = libra.libra_kv_layout_create(k, v, P, hkv)
+    bt = torch.from_numpy(rng.permutation(P)[:B * max_pages].astype(np.int32)
+                          .reshape(B, max_pages)).to(dev)
+    q = randn_i16(B * hq * 128)
+    out = torch.empty(B * hq * 128, dtype=torch.int16, device=dev)
+    lse = torch.empty(B * hq, dtype=torch.float32, device=dev)
+    dec = []
+    for L in CE_DECODE_LENS:
+        plan = libra.libra_splitkv_plan(libra.LIBRA_MODE_DECODE, B, hq, hkv, [L] * B)
+        ws = libra.alloc_workspace(plan)
+        libra.libra_plan_upload(plan, ws, stream=stream)
+        ms = timed(lambda: libra.libra_decode_attn(layout, plan, q, bt, max_pages, B, hq,
+                                                   0.088, ws, out, lse, stream=stream))
+        libra.libra_plan_destroy(plan)
+        dec.append(ms)
+        log(f"[bench] ce decode L={L}: {ms:.4f} ms")
+    libra.libra_kv_layout_destroy(layout)
+    del k, v
+    # (b) recompute prefill
+    P2 = max_pages + 1
+    k2 = randn_i16(P2 * hkv * 2048)
+    v2 = randn_i16(P2 * hkv * 2048)
+    layout2 = libra.libra_kv_layout_create(k2, v2, P2, hkv)
+    bt2 = torch.from_numpy(rng.permutation(P2)[:max_pages].astype(np.int32)[None, :]).to(dev)
+    qp = randn_i16(40960 * hq * 128)
+    kn = randn_i16(40960 * hkv * 128)
+    vn = randn_i16(40960 * hkv * 128)
+    outp = torch.empty(40960 * hq * 128, dtype=torch.int16, device=dev)
+    lsep = torch.empty(40960 * hq, dtype=torch.float32, device=dev)
+    pf, pf_chunk = [], []
+    for L in CE_PREFILL_LENS:
+        plan = libra.libra_splitkv_plan(libra.LIBRA_MODE_APPEND, 1, hq, hkv, [L], [L])
+        ws = libra.alloc_workspace(plan)
+        libra.libra_plan_upload(plan, ws, stream=stream)
+        call = lambda: libra.libra_append_attn(layout2, plan, qp, kn, vn, bt2, max_pages, 1, hq,
+                                               0.088, ws, outp, lsep, stream=stream)
+        ms = timed(call)
+        libra.libra_profile_enable(True)
+        libra.libra_profile_collect()
+        for _ in range(3):
+            call()
+        stream.synchronize()
+        kt = libra.libra_profile_collect()
+        libra.libra_profile_enable(False)
+        libra.libra_plan_destroy(plan)
+        pf.append(ms)
+        pf_chunk.append(kt["chunk"][0] / max(1, kt["chunk"][1]))
+        log(f"[bench] ce prefill L={L}: {ms:.4f} ms")
+    libra.libra_kv_layout_destroy(layout2)
+
+    def fit_report(lens, times):
+        lens = np.asarray(lens, dtype=np.float64)
+        times = np.asarray(times, dtype=np.float64)
+        train, held = lens[0::2], lens[1::2]
+        tt, th = times[0::2], times[1::2]
+        c_train = libra.libra_ce_fit(train, tt)
+        c_all = libra.libra_ce_fit(lens, times)
+        pred = c_all[0] * lens ** 2 + c_all[1] * lens + c_all[2]
+        return {"gamma_eta_theta": list(c_all),
+                "mape_heldout_pct": round(libra.libra_ce_mape(c_train, held, th), 3),
+                "mape_all_pct": round(libra.libra_ce_mape(c_all, lens, times), 3),
+                "points": [[int(L), round(float(t), 5), round(float(p), 5)]
+                           for L, t, p in zip(lens, times, pred)]}
+
+    d = fit_report(CE_DECODE_LENS, dec)
+    f = fit_report(CE_PREFILL_LENS, pf)
+    L = 40960
+    fl = 4 * 128 * hq * (L * (L + 1) // 2)
+    achieved = fl / (pf_chunk[-1] * 1e-3) / 1e12
+    # per-sequence attention of one decode step at context l (the rollout model's input)
+    per_seq = [c / B for c in d["gamma_eta_theta"]]
+    result = {
+        "metric": "cost-evaluator attention polynomial MAPE on held-out lengths",
+        "value": round(max(d["mape_heldout_pct"], f["mape_heldout_pct"]), 3),
+        "unit": "%", "n_gpus": 1, "steps": reps, "warmup": args.warmup,
+        "ms_per_step": round(pf[-1], 4),
+        "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (device-seeded normal bf16)",
+        "config": {"workload": "ce: per-layer attention of a 40-query / 8-KV-head model; decode "
+                               f"steps of {B} sequences at L in {CE_DECODE_LENS}; recompute "
+                               f"prefill of one sequence at L in {CE_PREFILL_LENS}"},
+        "decode_step": d, "prefill": f,
+        "attn_step_per_sequence": per_seq,
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 2),
+                     "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None,
+                     "kernel": "chunk_kernel (prefill, L = 40960)",
+                     "kernel_avg_ms": round(pf_chunk[-1], 5)},
+    }
+    if not args.no_cpu_baseline:
+        import oracle.cost_model as ocm
+        n, t0 = 0, time.perf_counter()
+        while time.perf_counter() - t0 < 1.0:
+            ocm.ce_fit_ref(CE_PREFILL_LENS, pf)
+            n += 1
+        el = time.perf_counter() - t0
+        result["cpu_baseline"] = {"value": round(n / el, 1), "unit": "fits/s", "cores": 1,
+                                  "kind": "oracle",
+                                  "sample": f"numpy least-squares fit of the prefill points x {n}"}
+    return result
+
+
+def bench_planner(args) -> dict:
+    """Host-side planner pieces: RolloutDP (Alg. 1) search time at cluster scale, literal
+    recurrence against the crossing search, and prefix-tree insert / lookup rates on
+    synthetic trajectories (Sec. 4.2, Sec. 5)."""
+    from paper_2606_03077_amd import libra
+    from paper_2606_03077_amd import workloads as wl
+    traces = wl.synthetic_traces(2000, 8, seed=26060)
+    lengths = np.array([r[0] for _, _, r in traces], dtype=np.int64)
+    # Model inputs, in seconds for a 40-layer model: the per-sequence decode attention
+    # step is 40 x the per-layer fit of the ce workload on MI355X (eta 6.87e-10 s per
+    # context token, theta 2.5e-7 s; its tiny negative gamma clipped to 0); the per-step
+    # non-attention time stands in for reading a 14B model's bf16 weights at each TP.
+    model = libra.rollout_model((0.0, 2.75e-8, 1.0e-5),
+                                {1: 3.5e-3, 2: 1.9e-3, 4: 1.05e-3, 8: 0.62e-3},
+                                {1: 1.0, 2: 0.52, 4: 0.27, 8: 0.15})
+    rows = []
+    for n_gpus, n_req, exact in [(8, 256, True), (8, 256, False), (64, 1024, True),
+                                 (64, 1024, False), (128, 1024, False), (128, 4096, False)]:
+        sub = lengths[:n_req]
+        t0 = time.perf_counter()
+        ms, _, inst = libra.libra_rollout_dp(sub, n_gpus, [1, 2, 4, 8], model, exact)
+        el = time.perf_counter() - t0
+        rows.append({"n_gpus": n_gpus, "n_req": n_req, "exact": exact, "search_s": round(el, 4),
+                     "makespan_s": round(ms, 3),
+                     "instances_per_tp": {str(t): sum(1 for tp, _, c in inst if tp == t)
+                                          for t in (8, 4, 2, 1)}})
+        log(f"[bench] planner {rows[-1]}")
+    tree = libra.PrefixTree([2048, 8192, 32768])
+    t0 = time.perf_counter()
+    for p, st, res in traces:
+        tree.insert(p, st, res)
+    ins = len(traces) / (time.perf_counter() - t0)
+    queries = [(p, st) for p, st, _ in traces]
+    t0 = time.perf_counter()
+    for p, st in queries:
+        tree.lookup(p, st)
+    look = len(queries) / (time.perf_counter() - t0)
+    tree.close()
+    big = next(r for r in rows if r["n_gpus"] == 128 and r["n_req"] == 1024)
+    result = {
+        "metric": "RolloutDP search time (128 GPUs, 1024 requests, TP set {1,2,4,8})",
+        "value": big["search_s"], "unit": "s", "n_gpus": 0, "steps": 1, "warmup": 0,
+        "ms_per_step": round(big["search_s"] * 1e3, 3),
+        "higher_is_better": False, "scaling": "strong", "vs_baseline": None, "dtype": "f64",
+        "data": "synthetic trajectories (workloads.synthetic_traces)",
+        "config": {"workload": "planner: host RolloutDP and prefix tree"},
+        "dp": rows,
+        "trie_inserts_per_s": round(ins, 1), "trie_lookups_per_s_python": round(look, 1),
+        "roofline": None,
+    }
+    if not args.no_cpu_baseline:
+        import oracle.cost_model as ocm
+        m = {"attn_step": (0.0, 2.75e-8, 1.0e-5),
+             "linear_step": [3.5e-3, 1.9e-3, 1.05e-3, 0.62e-3],
+             "attn_scale": [1.0, 0.52, 0.27, 0.15]}
+        sub = lengths[:24].tolist()
+        t0 = time.perf_counter()
+        ocm.rollout_dp_ref(sub, 8, [1, 2, 4, 8], m)
+        el = time.perf_counter() - t0
+        t1 = time.perf_counter()
+        libra.libra_rollout_dp(sub, 8, [1, 2, 4, 8], model, True)
+        el_lib = time.perf_counter() - t1
+        result["cpu_baseline"] = {"value": round(el, 4), "unit": "s", "cores": 1,
+                                  "kind": "oracle",
+                                  "sample": f"Alg. 1 in Python, 8 GPUs x 24 requests "
+                                            f"(library, same case: {el_lib:.5f} s)"}
+    return result
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -322,7 +539,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="7b",
                     choices=["tiny", "7b", "longtail", "straggler", "append", "prefill",
-                             "migrate"])
+                             "migrate", "ce", "planner"])
     ap.add_argument("--migrate-tokens", type=int, default=40960,
                     help="migrate workload: prefix length of the migrated request")
     ap.add_argument("--migrate-tp", default="1,2",
@@ -342,6 +559,11 @@ def main():
         print("bench.py measures one GPU: this build has no multi-GPU path "
               "(run with --gpus 1)", file=sys.stderr)
         sys.exit(2)
+
+    if args.workload == "planner":
+        sys.path.insert(0, ROOT)
+        print(json.dumps(bench_planner(args)), flush=True)
+        return
 
     import torch
     if args.copy_calibration:
@@ -366,6 +588,9 @@ def main():
     torch.cuda.set_device(dev)
     if args.workload == "migrate":
         print(json.dumps(bench_migrate(args, torch, libra, wl)), flush=True)
+        return
+    if args.workload == "ce":
+        print(json.dumps(bench_ce(args, torch, libra)), flush=True)
         return
 
     log(f"[bench] generating workload {args.workload}")

@@ -320,6 +320,124 @@ typedef struct libra_kernel_times {
 libra_status libra_profile_enable(int enable);
 libra_status libra_profile_collect(libra_kernel_times* out);
 
+/* ------------------------------------------------------------------------------ */
+/* Cost evaluator: per-operator latency polynomials (host)                         */
+/* ------------------------------------------------------------------------------ */
+/*
+ * The cost evaluator models the time of an operator at sequence length L as a
+ * polynomial, quadratic for attention, T(L) = gamma L^2 + eta L + theta, whose
+ * coefficients come from timings measured offline (Sec. 4.5; App. B.1, "CE
+ * calibration").  Its fidelity is reported as the mean absolute percentage error (MAPE)
+ * of predicted against measured times (Sec. 7.5).  All functions here are pure host
+ * arithmetic on caller memory.
+ */
+typedef struct libra_ce_poly {
+  double gamma; /* coefficient of L^2 */
+  double eta;   /* coefficient of L */
+  double theta; /* constant */
+} libra_ce_poly;
+
+/* Least-squares fit of T(L) to n measured points (lengths[i], times[i]), minimising the
+ * sum of squared RELATIVE errors ((T(L_i) - t_i) / t_i)^2, the quantity MAPE averages.
+ * Needs n >= 3, at least 3 distinct lengths, finite lengths >= 0 and finite times > 0;
+ * otherwise LIBRA_E_INVAL. */
+libra_status libra_ce_fit(const double* lengths, const double* times, int32_t n,
+                          libra_ce_poly* out);
+
+/* MAPE in percent: 100 / n * sum |T(L_i) - t_i| / t_i (times > 0, n >= 1). */
+libra_status libra_ce_mape(const libra_ce_poly* poly, const double* lengths, const double* times,
+                           int32_t n, double* mape);
+
+/* Sum of T(l) over the integers l = a .. b (0 if b < a), in closed form: the time of a
+ * decode trajectory whose per-step operator time at context l is T(l).  Needs
+ * 0 <= a, b <= 2^24. */
+libra_status libra_ce_poly_sum(const libra_ce_poly* poly, int64_t a, int64_t b, double* out);
+
+/* ------------------------------------------------------------------------------ */
+/* Rollout partition: RolloutDP (host)                                             */
+/* ------------------------------------------------------------------------------ */
+/*
+ * Splits n_gpus GPUs into inference instances of TP degrees from a set (e.g. {1,2,4,8})
+ * and gives each instance a contiguous run of the requests sorted by length, minimising
+ * the makespan (Sec. 4.2; Alg. 1, RolloutDP):
+ *
+ *   dp[0][0] = 0, dp[g][i] = min over tp <= g, 0 <= x <= i of
+ *              max(dp[g - tp][i - x], Cost(tp, i - x + 1, i)),     answer dp[n_gpus][n_req].
+ *
+ * Cost(tp, a, b) is the cost evaluator's RolloutTime of one instance serving sorted
+ * requests a..b (1-based; empty when x = 0, cost 0).  The library's model of it (the
+ * paper leaves the aggregation to its simulator) is continuous batching of all the
+ * instance's requests: the instance runs as many decode steps as its longest request,
+ * each paying the non-attention time once, and every request pays its own trajectory's
+ * attention time:
+ *
+ *   Cost(tp, a, b) = linear_step[tp] * len_b + attn_scale[tp] * sum_{j=a..b} A(len_j),
+ *   A(len) = sum_{l=1..len} attn_step(l)          (libra_ce_poly_sum(attn_step, 1, len)).
+ *
+ * Ties: candidates are visited in increasing g, i, then tp in tp_set order, then x
+ * ascending, and a candidate replaces the best only when strictly smaller.
+ */
+typedef struct libra_rollout_model {
+  libra_ce_poly attn_step; /* attention time of one decode step of one request at context l */
+  double linear_step[4];   /* non-attention time per decode step of an instance at TP 1,2,4,8 */
+  double attn_scale[4];    /* attention time multiplier at TP 1, 2, 4, 8 */
+} libra_rollout_model;
+
+/* lengths: n_req request lengths (>= 0, <= 2^24).  tp_set: n_tp distinct degrees from
+ * {1, 2, 4, 8}.  Outputs: *makespan (+inf if no partition uses exactly n_gpus GPUs);
+ * order[n_req] = request indices sorted by (length, index); instances[3 * k] =
+ * (tp, first sorted position, count) for the k-th instance, in backtracking order
+ * (last-added first), *n_instances <= n_gpus.  Work O(n_gpus * n_req^2 * n_tp) with the
+ * literal recurrence (exact = 1), or O(n_gpus * n_req * n_tp * log n_req) (exact = 0),
+ * which uses that both arguments of the max are monotone in x and returns the same
+ * makespan.  Limits: n_gpus <= 4096, n_req <= 65536. */
+libra_status libra_rollout_dp(const int64_t* lengths, int32_t n_req, int32_t n_gpus,
+                              const int32_t* tp_set, int32_t n_tp,
+                              const libra_rollout_model* model, int32_t exact, double* makespan,
+                              int32_t* order, int32_t* instances, int32_t* n_instances);
+
+/* ------------------------------------------------------------------------------ */
+/* Causality-guided bucket routing (host)                                          */
+/* ------------------------------------------------------------------------------ */
+/*
+ * A prefix tree over tool-return histories (Sec. 5, "Causality-aware prefix tree").  A
+ * node at depth k is the key (prompt_id, <s_1 .. s_k>), where s_i is the composite state
+ * of the i-th tool call (tool type, payload size class, success or failure; encode it
+ * with LIBRA_TOOL_STATE).  Every node counts the remaining trajectory length observed
+ * from that point, in bins aligned to the bucket length thresholds: bin k holds lengths
+ * in [edge[k-1], edge[k]) with edge[-1] = 0 and edge[n_edges] = infinity, so there are
+ * n_edges + 1 bins.  A root above all prompts (depth -1) gathers every trace.
+ */
+#define LIBRA_TOOL_STATE(tool_type, large, failure) \
+  ((int32_t)(((tool_type) << 2) | ((large) ? 2 : 0) | ((failure) ? 1 : 0)))
+
+typedef struct libra_trie_s* libra_trie;
+
+/* bin_edges: n_edges strictly increasing positive thresholds (n_edges in [0, 63]). */
+libra_status libra_trie_create(const int64_t* bin_edges, int32_t n_edges, libra_trie* out);
+void libra_trie_destroy(libra_trie trie);
+
+/* Inserts one finished trajectory (Sec. 5, Phase 3; App. B.1 bootstrap): states[0 ..
+ * n_states) are its tool returns in order, residual[k] (k = 0 .. n_states) the length
+ * still to be generated after the k-th return (residual[0]: from the prompt on).  The
+ * root, the prompt node and the node after each return record their residual. */
+libra_status libra_trie_insert(libra_trie trie, int64_t prompt_id, const int32_t* states,
+                               int32_t n_states, const int64_t* residual);
+
+/* Walks (prompt_id, states[0 .. n_states)) and writes the residual-length distribution
+ * F = {p_k} of the deepest node on that path that exists (an unseen node backs off to
+ * its parent; an unseen prompt to the root) into hist[n_edges + 1], and that node's
+ * depth into *depth (-1 = root).  An empty tree gives LIBRA_E_INVAL. */
+libra_status libra_trie_lookup(libra_trie trie, int64_t prompt_id, const int32_t* states,
+                               int32_t n_states, double* hist, int32_t* depth);
+
+/* Phase 2 routing (Sec. 5): B* = argmin_B sum_k hist[k] * t_dec[B * n_bins + k] +
+ * c_mig[current * n_buckets + B], with c_mig's diagonal taken as 0 whatever it holds.
+ * Ties go to the lowest bucket index.  Writes *best and its cost *best_cost. */
+libra_status libra_route_bucket(const double* hist, int32_t n_bins, const double* t_dec,
+                                const double* c_mig, int32_t n_buckets, int32_t current,
+                                int32_t* best, double* best_cost);
+
 #ifdef __cplusplus
 }
 #endif

@@ -35,3 +35,7 @@ from .attention import (  # noqa: F401
 )
 from .plan import plan_ref, PlanParams, UNIT_FIELDS  # noqa: F401
 from .migration import reshard_heads, request_pages, query_heads_of_shard  # noqa: F401
+from .cost_model import (  # noqa: F401
+    ce_fit_ref, mape_ref, poly_sum_ref, instance_cost, rollout_dp_ref, partition_makespan,
+)
+from .scheduler import PrefixTreeRef, route_ref  # noqa: F401

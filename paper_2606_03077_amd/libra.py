@@ -34,7 +34,10 @@ EXPORTS = ("libra_status_string", "libra_last_error", "libra_kv_layout_create",
            "libra_splitkv_plan", "libra_plan_get_units", "libra_plan_get_info",
            "libra_plan_workspace_bytes", "libra_plan_upload", "libra_plan_destroy",
            "libra_decode_attn", "libra_append_attn", "libra_profile_enable",
-           "libra_profile_collect")
+           "libra_profile_collect", "libra_ce_fit", "libra_ce_mape", "libra_ce_poly_sum",
+           "libra_rollout_dp", "libra_trie_create", "libra_trie_destroy", "libra_trie_insert",
+           "libra_trie_lookup", "libra_route_bucket")
+TP_SLOTS = {1: 0, 2: 1, 4: 2, 8: 3}
 KERNEL_KINDS = ("pack", "unpack", "gather", "cache_write", "decode", "merge", "chunk", "upload",
                 "copy_out", "copy_in")
 
@@ -71,6 +74,15 @@ class PlanInfo(ctypes.Structure):
                 ("num_cus", ctypes.c_int32), ("n_merge_groups", ctypes.c_int32)]
 
 
+class CePoly(ctypes.Structure):
+    _fields_ = [("gamma", ctypes.c_double), ("eta", ctypes.c_double), ("theta", ctypes.c_double)]
+
+
+class RolloutModel(ctypes.Structure):
+    _fields_ = [("attn_step", CePoly), ("linear_step", ctypes.c_double * 4),
+                ("attn_scale", ctypes.c_double * 4)]
+
+
 class KernelTimes(ctypes.Structure):
     _fields_ = [("ms", ctypes.c_double * len(KERNEL_KINDS)),
                 ("launches", ctypes.c_int64 * len(KERNEL_KINDS))]
@@ -94,6 +106,8 @@ def load() -> ctypes.CDLL:
     lib = ctypes.CDLL(_LIB_PATH)
     P, I32, I64, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
     I32P = ctypes.POINTER(ctypes.c_int32)
+    I64P = ctypes.POINTER(ctypes.c_int64)
+    DP = ctypes.POINTER(ctypes.c_double)
     sig = {
         "libra_status_string": (ctypes.c_char_p, [ctypes.c_int]),
         "libra_last_error": (ctypes.c_char_p, []),
@@ -119,6 +133,17 @@ def load() -> ctypes.CDLL:
                                              SZ, P, P, P]),
         "libra_profile_enable": (ctypes.c_int, [ctypes.c_int]),
         "libra_profile_collect": (ctypes.c_int, [ctypes.POINTER(KernelTimes)]),
+        "libra_ce_fit": (ctypes.c_int, [DP, DP, I32, ctypes.POINTER(CePoly)]),
+        "libra_ce_mape": (ctypes.c_int, [ctypes.POINTER(CePoly), DP, DP, I32, DP]),
+        "libra_ce_poly_sum": (ctypes.c_int, [ctypes.POINTER(CePoly), I64, I64, DP]),
+        "libra_rollout_dp": (ctypes.c_int, [I64P, I32, I32, I32P, I32,
+                                            ctypes.POINTER(RolloutModel), I32, DP, I32P, I32P,
+                                            I32P]),
+        "libra_trie_create": (ctypes.c_int, [I64P, I32, ctypes.POINTER(P)]),
+        "libra_trie_destroy": (None, [P]),
+        "libra_trie_insert": (ctypes.c_int, [P, I64, I32P, I32, I64P]),
+        "libra_trie_lookup": (ctypes.c_int, [P, I64, I32P, I32, DP, I32P]),
+        "libra_route_bucket": (ctypes.c_int, [DP, I32, DP, DP, I32, I32, I32P, DP]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -262,6 +287,8 @@ def libra_splitkv_plan(mode: int, batch: int, num_q_heads: int, num_kv_heads: in
     sl = _i32_array(seq_lens)
     ql = None if q_lens is None else _i32_array(q_lens)
     I32P = ctypes.POINTER(ctypes.c_int32)
+    I64P = ctypes.POINTER(ctypes.c_int64)
+    DP = ctypes.POINTER(ctypes.c_double)
     h = ctypes.c_void_p()
     _check(load().libra_splitkv_plan(ctypes.byref(d), sl.ctypes.data_as(I32P),
                                      None if ql is None else ql.ctypes.data_as(I32P),
@@ -335,3 +362,137 @@ def alloc_workspace(plan: int, device="cuda") -> torch.Tensor:
     if ws.data_ptr() % 256:
         raise RuntimeError("torch returned a workspace that is not 256-byte aligned")
     return ws
+
+
+# --- cost evaluator, rollout DP, prefix tree and routing (host only) ----------------
+
+def _f64(x) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(x, dtype=np.float64))
+
+
+def _i64(x) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(x, dtype=np.int64))
+
+
+def _dp(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
+
+
+def _i32p(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+
+
+def _i64p(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_int64))
+
+
+def _poly(p) -> CePoly:
+    if isinstance(p, CePoly):
+        return p
+    g, e, t = p
+    return CePoly(float(g), float(e), float(t))
+
+
+def libra_ce_fit(lengths, times):
+    """(gamma, eta, theta) of T(L) = gamma L^2 + eta L + theta, least squares in relative error."""
+    L, T = _f64(lengths), _f64(times)
+    if L.shape != T.shape:
+        raise ValueError("lengths and times differ in size")
+    out = CePoly()
+    _check(load().libra_ce_fit(_dp(L), _dp(T), len(L), ctypes.byref(out)), "libra_ce_fit")
+    return out.gamma, out.eta, out.theta
+
+
+def libra_ce_mape(poly, lengths, times) -> float:
+    L, T = _f64(lengths), _f64(times)
+    m = ctypes.c_double()
+    pp = _poly(poly)
+    _check(load().libra_ce_mape(ctypes.byref(pp), _dp(L), _dp(T), len(L), ctypes.byref(m)),
+           "libra_ce_mape")
+    return m.value
+
+
+def libra_ce_poly_sum(poly, a: int, b: int) -> float:
+    out = ctypes.c_double()
+    pp = _poly(poly)
+    _check(load().libra_ce_poly_sum(ctypes.byref(pp), a, b, ctypes.byref(out)),
+           "libra_ce_poly_sum")
+    return out.value
+
+
+def rollout_model(attn_step, linear_step: dict, attn_scale: dict) -> RolloutModel:
+    """linear_step / attn_scale map a TP degree (1, 2, 4, 8) to its figure."""
+    m = RolloutModel()
+    m.attn_step = _poly(attn_step)
+    for tp, slot in TP_SLOTS.items():
+        m.linear_step[slot] = float(linear_step.get(tp, 0.0))
+        m.attn_scale[slot] = float(attn_scale.get(tp, 0.0))
+    return m
+
+
+def libra_rollout_dp(lengths, n_gpus: int, tp_set, model: RolloutModel, exact: bool = True):
+    """Returns (makespan, order, instances) with instances a list of (tp, first, count)."""
+    L = _i64(lengths)
+    tps = _i32_array(tp_set)
+    order = np.zeros(max(1, len(L)), dtype=np.int32)
+    inst = np.zeros(3 * max(1, n_gpus), dtype=np.int32)
+    k = ctypes.c_int32()
+    ms = ctypes.c_double()
+    _check(load().libra_rollout_dp(_i64p(L), len(L), n_gpus, _i32p(tps), len(tps),
+                                   ctypes.byref(model), int(bool(exact)), ctypes.byref(ms),
+                                   _i32p(order), _i32p(inst), ctypes.byref(k)),
+           "libra_rollout_dp")
+    return ms.value, order[:len(L)].copy(), [tuple(int(v) for v in inst[3 * j:3 * j + 3])
+                                              for j in range(k.value)]
+
+
+class PrefixTree:
+    """Owns a libra_trie handle (residual-length histograms over tool-return histories)."""
+
+    def __init__(self, bin_edges):
+        e = _i64(bin_edges)
+        self.n_bins = len(e) + 1
+        h = ctypes.c_void_p()
+        _check(load().libra_trie_create(_i64p(e) if len(e) else None, len(e), ctypes.byref(h)),
+               "libra_trie_create")
+        self.handle = h
+
+    def insert(self, prompt_id: int, states, residual):
+        st, r = _i32_array(states), _i64(residual)
+        if len(r) != len(st) + 1:
+            raise ValueError("residual needs one entry per state plus one")
+        _check(load().libra_trie_insert(self.handle, prompt_id, _i32p(st), len(st), _i64p(r)),
+               "libra_trie_insert")
+
+    def lookup(self, prompt_id: int, states):
+        st = _i32_array(states)
+        hist = np.zeros(self.n_bins, dtype=np.float64)
+        d = ctypes.c_int32()
+        _check(load().libra_trie_lookup(self.handle, prompt_id, _i32p(st), len(st), _dp(hist),
+                                        ctypes.byref(d)), "libra_trie_lookup")
+        return hist, d.value
+
+    def close(self):
+        if self.handle:
+            load().libra_trie_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def libra_route_bucket(hist, t_dec, c_mig, current: int):
+    """(best bucket, its cost); t_dec is [buckets][bins], c_mig [buckets][buckets]."""
+    h, td, cm = _f64(hist), _f64(t_dec), _f64(c_mig)
+    M = td.shape[0]
+    if td.shape != (M, len(h)) or cm.shape != (M, M):
+        raise ValueError("t_dec must be [buckets][bins] and c_mig [buckets][buckets]")
+    best = ctypes.c_int32()
+    cost = ctypes.c_double()
+    _check(load().libra_route_bucket(_dp(h), len(h), _dp(td), _dp(cm), M, current,
+                                     ctypes.byref(best), ctypes.byref(cost)),
+           "libra_route_bucket")
+    return best.value, cost.value

@@ -293,3 +293,50 @@ def custom_batch(seq_lens, q_lens=None, num_q_heads=8, num_kv_heads=2, seed=0,
                  append=append)
     rng = np.random.default_rng(seed)
     return build_batch(w, seq_lens, q_lens, rng, spare_frac=spare_frac, poison=poison)
+
+
+# --- synthetic agentic trajectories (stand-ins for the paper's rollout logs) ---------
+
+def tool_state(tool_type: int, large: bool, failure: bool) -> int:
+    """Composite tool-return state: tool type x payload size class x outcome."""
+    return (int(tool_type) << 2) | (2 if large else 0) | (1 if failure else 0)
+
+
+def synthetic_traces(n_prompts: int, per_prompt: int, seed: int = 2606, n_tool_types: int = 4):
+    """Seeded multi-turn trajectories: (prompt_id, states, residual) per trace.
+
+    Each prompt has a base difficulty; a trajectory alternates reasoning segments and
+    tool calls until it stops.  Failed tools make another call more likely and add
+    tokens (retries), large payloads add a long appended output, mirroring the paper's
+    observation that payload size and tool failures drive length (Sec. 1, Sec. 2.2).
+    ``residual[k]`` is the number of tokens still to come after the k-th tool return
+    (``residual[0]`` counts from the prompt on).
+    """
+    rng = np.random.default_rng(seed)
+    traces = []
+    for p in range(n_prompts):
+        difficulty = rng.lognormal(0.0, 0.6)
+        p_fail = min(0.8, 0.15 * difficulty)
+        for _ in range(per_prompt):
+            segments = [int(rng.lognormal(6.0, 0.5) * difficulty)]
+            states = []
+            p_more = 0.7
+            while rng.random() < p_more and len(states) < 24:
+                t = int(rng.integers(n_tool_types))
+                large = bool(rng.random() < 0.3)
+                fail = bool(rng.random() < p_fail)
+                states.append(tool_state(t, large, fail))
+                seg = int(rng.lognormal(5.5, 0.6) * difficulty)
+                if large:
+                    seg += int(rng.lognormal(7.5, 0.4))
+                if fail:
+                    seg += int(rng.lognormal(6.5, 0.5))
+                    p_more = min(0.95, p_more + 0.1)
+                else:
+                    p_more = max(0.2, p_more - 0.15)
+                segments.append(seg)
+            total = int(sum(segments))
+            done = np.cumsum([0] + segments[:-1])[:len(states) + 1]
+            residual = [total - int(d) for d in done]
+            traces.append((p, states, residual))
+    return traces

@@ -123,3 +123,70 @@ def test_reshard_mutants_are_caught(monkeypatch, mutant):
     caught = [_caught(mig.test_split_by_brute_force), _caught(mig.test_join_by_brute_force),
               _caught(mig.test_shard_decode_reproduces_full_heads, 32, 8, 4)]
     assert any(caught), caught
+
+
+# --- cost evaluator, RolloutDP, prefix tree, routing --------------------------------
+
+def test_unweighted_fit_is_caught(monkeypatch):
+    import test_cost_model_oracle as cm
+
+    def absolute_fit(lengths, times):
+        L = np.asarray(lengths, dtype=np.float64)
+        A = np.stack([L * L, L, np.ones_like(L)], axis=1)
+        coef, *_ = np.linalg.lstsq(A, np.asarray(times, dtype=np.float64), rcond=None)
+        return tuple(float(c) for c in coef)
+
+    monkeypatch.setattr(cm, "ce_fit_ref", absolute_fit)
+    assert _caught(cm.test_fit_normal_equations_hold)
+
+
+def test_dp_segment_off_by_one_is_caught(monkeypatch):
+    import oracle.cost_model as ocm
+    import test_cost_model_oracle as cm
+    real = ocm.instance_cost
+
+    def dp_with_wrong_segment(lengths, n_gpus, tp_set, model):
+        order = ocm.sorted_order(lengths)
+        ls = [int(lengths[j]) for j in order]
+        n = len(ls)
+        dp = [[np.inf] * (n + 1) for _ in range(n_gpus + 1)]
+        dp[0][0] = 0.0
+        for g in range(1, n_gpus + 1):
+            for i in range(n + 1):
+                for tp in tp_set:
+                    if tp > g:
+                        continue
+                    for x in range(i + 1):
+                        seg = ls[max(0, i - x - 1):i] if x else []   # one request too many
+                        dp[g][i] = min(dp[g][i], max(dp[g - tp][i - x], real(model, tp, seg)))
+        return dp[n_gpus][n], order, []
+
+    monkeypatch.setattr(cm, "rollout_dp_ref", dp_with_wrong_segment)
+    assert any(_caught(cm.test_rollout_dp_equals_brute_force, s) for s in range(6))
+
+
+def test_trie_back_off_to_root_is_caught(monkeypatch):
+    import oracle.scheduler as osch
+    import test_scheduler_oracle as so
+    real = osch.PrefixTreeRef.lookup
+
+    def lookup_root_on_miss(self, prompt_id, states):
+        h, d = real(self, prompt_id, states)
+        if d < len(states) and d >= 0:
+            return real(self, -12345, [])
+        return h, d
+
+    monkeypatch.setattr(osch.PrefixTreeRef, "lookup", lookup_root_on_miss)
+    assert _caught(so.test_back_off_to_parent)
+
+
+def test_route_without_migration_cost_is_caught(monkeypatch):
+    import test_scheduler_oracle as so
+
+    def route_free_moves(hist, t_dec, c_mig, current):
+        costs = [sum(h * t for h, t in zip(hist, row)) for row in t_dec]
+        b = min(range(len(costs)), key=lambda i: (costs[i], i))
+        return b, costs[b]
+
+    monkeypatch.setattr(so, "route_ref", route_free_moves)
+    assert _caught(so.test_route_by_hand)
