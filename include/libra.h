@@ -13,12 +13,17 @@
  * ---------------------------------
  * - All tensors are borrowed pointers owned by the caller.  "device" pointers must be
  *   HIP device memory of the current device; "host" pointers are ordinary host memory.
- * - Handles (libra_kv_layout, libra_plan) are created and destroyed by the library and
- *   are immutable after creation, except that a plan remembers which workspace its
- *   tables were last uploaded to.
+ * - Handles (libra_kv_layout, libra_plan, libra_trie) are created and destroyed by the
+ *   library.  Layouts and plans are immutable after creation, except that a plan
+ *   remembers which workspace its tables were last uploaded to; a prefix tree grows by
+ *   libra_trie_insert and must not be inserted into while another thread uses it.
  * - Work is enqueued asynchronously on `stream` (a hipStream_t; NULL = the null stream).
  *   No entry point synchronises the device or allocates device memory, except
- *   libra_plan_destroy, which waits for its own pending upload.
+ *   libra_plan_destroy, which waits for its own pending upload.  A plan's first upload
+ *   allocates its pinned host copy of the tables (freed by libra_plan_destroy).
+ * - Host-only entry points (plan construction, cost evaluator, RolloutDP, prefix tree,
+ *   routing, libra_kv_reshard_host) touch no GPU; the reshard may use up to 8 host
+ *   threads for large runs.
  * - Every entry point returns a libra_status; nothing aborts, prints or throws.  On an
  *   error nothing has been enqueued, and libra_last_error() gives a per-thread message.
  * - Validation happens on the host before any launch.  Device-side contract violations

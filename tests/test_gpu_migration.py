@@ -247,3 +247,49 @@ def test_direct_pcie_runs_match_staged():
     assert "pinned" in str(e.value)
     dst.close()
     src.close()
+
+
+@pytest.mark.parametrize("n_dst", [1, 2, 4])
+def test_decode_after_reload_equals_before(n_dst):
+    """Decode on the migrated shards is bit-identical to decode on the source cache, for
+    each shard's query heads, when both run one unit per (sequence, KV head): every head's
+    unit then reads the same key tiles in the same order and does the same arithmetic."""
+    say(f"[case] decode after reload equals before, TP1->TP{n_dst}")
+    hq, hkv = 32, 8
+    batch = wl.custom_batch([2000], num_q_heads=hq, num_kv_heads=hkv, seed=77 + n_dst)
+    L = int(batch.seq_lens[0])
+    n = -(-L // 16)
+    src = DeviceCache(batch)
+    no_split = dict(min_split_pages=1 << 20, max_splits=1)
+    ids_np = np.ascontiguousarray(batch.block_table[0, :n])
+
+    def decode(layout, heads_q, heads_kv, bt_row, q_rows):
+        plan = libra.libra_splitkv_plan(libra.LIBRA_MODE_DECODE, 1, heads_q, heads_kv, [L], None,
+                                        **no_split)
+        try:
+            assert libra.libra_plan_get_info(plan)["n_partial_slots"] == 0
+            ws = libra.alloc_workspace(plan)
+            bt = torch.from_numpy(np.ascontiguousarray(bt_row[None, :])).cuda()
+            out = torch.empty((1, heads_q, 128), dtype=torch.int16, device="cuda")
+            lse = torch.empty((1, heads_q), dtype=torch.float32, device="cuda")
+            libra.libra_decode_attn(layout, plan, u16_to_dev(q_rows), bt, bt.shape[1], 1, heads_q,
+                                    batch.scale, ws, out, lse)
+            torch.cuda.synchronize()
+            return dev_to_u16(out), lse.cpu().numpy()
+        finally:
+            libra.libra_plan_destroy(plan)
+
+    o_before, l_before = decode(src.layout, hq, hkv, ids_np, batch.q[0:1])
+    targets, tids = migrate([src.layout], hkv, [torch.from_numpy(ids_np).cuda()], n, n_dst,
+                            dst_pages=n + 7, seed=3)
+    try:
+        for j, (c, t) in enumerate(zip(targets, tids)):
+            qh = query_heads_of_shard(j, n_dst, hq)
+            o, l = decode(c.layout, hq // n_dst, hkv // n_dst, t,
+                          np.ascontiguousarray(batch.q[0:1, qh]))
+            assert np.array_equal(o, o_before[:, qh]), f"shard {j}: output differs"
+            assert np.array_equal(l, l_before[:, qh]), f"shard {j}: lse differs"
+    finally:
+        for c in targets:
+            c.close()
+        src.close()
