@@ -4,8 +4,9 @@
 // [q0, q1)).  Query rows are (token, head) pairs of the G heads sharing KV head g, packed
 // into 16-wide matrix columns, tpb = max(1, 16 / G) tokens per column block; each wave
 // owns 2 column blocks, so a workgroup covers up to 16 * tpb tokens.  Keys are visited
-// 64 at a time: the step's eight 4 KiB tiles (K and V of 4 pages) are staged in LDS
-// (three stages) and shared by the 8 waves; V is interleaved by page pair on the way
+// 64 at a time: the step's eight 4 KiB tiles (K and V of 4 pages) are loaded into
+// registers two steps ahead, staged in LDS (three stages) and shared by the 8 waves; V
+// is interleaved by page pair on the way
 // in so that each PV operand is a single 16-byte LDS read.  Each wave computes the
 // next step's scores while it turns the current step's into probabilities.  Per page and column block:
 //   S^T = K . Q^T (4 mfma 16x16x32), and per page pair O^T += V^T . P^T (8 mfma 16x16x32
@@ -290,39 +291,58 @@ void chunk_kernel(ChunkArgs A) {
   // formed and multiplied into V, step n + 1's scores are computed from its K (the two
   // are independent, so matrix and vector work interleave within each wave) and step
   // n + 2 is in flight from memory.
-  uint4 stage[kStepPages];
+  // Staging registers come in two sets: step n + 3 is loaded into one while step n + 2,
+  // loaded a whole step earlier, waits in the other to be written to LDS at the end of
+  // step n, so each load has two steps of compute to land.
+  uint4 stage_a[kStepPages], stage_b[kStepPages];
   if (nsteps > 0) {
-    fetch(0, stage);
-    stash(0, stage);
+    fetch(0, stage_a);
+    stash(0, stage_a);
   }
   if (nsteps > 1) {
-    fetch(1, stage);
-    stash(1, stage);
+    fetch(1, stage_a);
+    stash(1, stage_a);
   }
   // Every load issued so far (Q operands, the first stages) has landed: the loop's
   // wait counts then only track the in-loop prefetch.
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
+  if (nsteps > 2) fetch(2, stage_a);
 
-  f32x4 s_cur[kStepPages][kNB], s_nxt[kStepPages][kNB];
-  if (nsteps > 0) qk(0, s_cur);
-  // Steps before the last: no V tail to clear, so exp, next scores and PV form one
-  // branch-free block the scheduler can interleave.
-  for (int n = 0; n + 1 < nsteps; ++n) {
+  f32x4 s_a[kStepPages][kNB], s_b[kStepPages][kNB];
+  if (nsteps > 0) qk(0, s_a);
+  // Every step before the last: no V tail to clear, so exp, next scores and PV form one
+  // branch-free block the scheduler can interleave.  `landing` holds step n + 2,
+  // `flying` receives step n + 3; the score and staging sets swap roles every step.
+  using Scores = f32x4[kStepPages][kNB];
+  using Stage = uint4[kStepPages];
+  auto step = [&](int n, Scores& s_cur, Scores& s_nxt, Stage& landing, Stage& flying) {
     const int key0 = n * kStepPages * kPage;
-    if (n + 2 < nsteps) fetch(n + 2, stage);
     float neg_m[kNB];
     prepare(key0, s_cur, neg_m);
     bf16x8 pop[kNB][2];
     exp_and_next_qk((n + 1) % kBufs, s_cur, neg_m, pop, s_nxt);
+    // Unconditional (the last steps re-load the final step's pages, unused), so that the
+    // wait before the stash below only ever counts this step's four loads as younger.
+    fetch(min(n + 3, nsteps - 1), flying);
     pv(n % kBufs, key0, pop, std::false_type{});
-    if (n + 2 < nsteps) stash((n + 2) % kBufs, stage);
+    if (n + 2 < nsteps) stash((n + 2) % kBufs, landing);
     __syncthreads();
+  };
+  int n0 = 0;
+  for (; n0 + 2 < nsteps; n0 += 2) {
+    step(n0, s_a, s_b, stage_a, stage_b);
+    step(n0 + 1, s_b, s_a, stage_b, stage_a);
+  }
+  if (n0 + 1 < nsteps) {
+    step(n0, s_a, s_b, stage_a, stage_b);
 #pragma unroll
     for (int j = 0; j < kStepPages; ++j)
 #pragma unroll
-      for (int nb = 0; nb < kNB; ++nb) s_cur[j][nb] = s_nxt[j][nb];
+      for (int nb = 0; nb < kNB; ++nb) s_a[j][nb] = s_b[j][nb];
   }
+  Scores& s_cur = s_a;
+  Scores& s_nxt = s_b;
   if (nsteps > 0) {
     const int n = nsteps - 1;
     const int key0 = n * kStepPages * kPage;
