@@ -15,8 +15,10 @@
  *   HIP device memory of the current device; "host" pointers are ordinary host memory.
  * - Handles (libra_kv_layout, libra_plan, libra_trie) are created and destroyed by the
  *   library.  Layouts and plans are immutable after creation, except that a plan
- *   remembers which workspace its tables were last uploaded to; a prefix tree grows by
- *   libra_trie_insert and must not be inserted into while another thread uses it.
+ *   remembers (under a lock) which workspace its tables were last uploaded to, so calls
+ *   on different streams with distinct workspaces and outputs may share a plan; a prefix
+ *   tree grows by libra_trie_insert and must not be inserted into while another thread
+ *   uses it.  A handle is destroyed only after the calls that use it were issued.
  * - Work is enqueued asynchronously on `stream` (a hipStream_t; NULL = the null stream).
  *   No entry point synchronises the device or allocates device memory, except
  *   libra_plan_destroy, which waits for its own pending upload.  A plan's first upload

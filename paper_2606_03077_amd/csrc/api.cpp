@@ -113,7 +113,10 @@ int64_t plan_pages_needed(const Plan& P) {
   return need;
 }
 
-libra_status upload(Plan& P, void* ws, size_t ws_bytes, hipStream_t s) {
+// Copies the plan's tables into ws unless ws already holds them (or always, if forced).
+libra_status upload(Plan& P, void* ws, size_t ws_bytes, hipStream_t s, bool force = true) {
+  std::lock_guard<std::mutex> lk(P.upload_mu);
+  if (!force && P.uploaded_ws == ws) return LIBRA_OK;
   if (!ws) return set_error(LIBRA_E_INVAL, "workspace is NULL");
   if (reinterpret_cast<uintptr_t>(ws) % kWorkspaceAlign)
     return set_error(LIBRA_E_INVAL, "workspace must be 256-byte aligned");
@@ -443,10 +446,8 @@ libra_status libra_decode_attn(libra_kv_layout layout, libra_plan plan, const vo
   if (ws_bytes < plan->ws_bytes)
     return set_error(LIBRA_E_WORKSPACE, "workspace smaller than libra_plan_workspace_bytes");
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if (plan->uploaded_ws != workspace) {
-    st = upload(*plan, workspace, ws_bytes, s);
-    if (st != LIBRA_OK) return st;
-  }
+  st = upload(*plan, workspace, ws_bytes, s, false);
+  if (st != LIBRA_OK) return st;
   return launch_attention(*layout, *plan, workspace, q, block_table, bt_stride, scale, out, lse, s);
 }
 
@@ -466,10 +467,8 @@ libra_status libra_append_attn(libra_kv_layout layout, libra_plan plan, const vo
   if (ws_bytes < plan->ws_bytes)
     return set_error(LIBRA_E_WORKSPACE, "workspace smaller than libra_plan_workspace_bytes");
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if (plan->uploaded_ws != workspace) {
-    st = upload(*plan, workspace, ws_bytes, s);
-    if (st != LIBRA_OK) return st;
-  }
+  st = upload(*plan, workspace, ws_bytes, s, false);
+  if (st != LIBRA_OK) return st;
   hipError_t e;
   {
     ProfScope ps(LIBRA_KERNEL_CACHE_WRITE, s, plan->info.n_write_tiles > 0);

@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -53,7 +54,8 @@ struct Plan {
   size_t ws_bytes = 0;
   size_t upload_bytes = 0;  // bytes of [units | writes | merges] copied from the host
 
-  // Upload state.
+  // Upload state (guarded by upload_mu: calls on one plan may come from several threads).
+  std::mutex upload_mu;
   void* pinned = nullptr;         // host staging copy of [units | writes | merges]
   hipEvent_t upload_done = nullptr;
   void* uploaded_ws = nullptr;

@@ -115,9 +115,19 @@ def errors(o, lse, ro, rl, rows=None):
     return max_abs, max_rel, max_lse
 
 
+def allclose_fraction(o, ro, rows=None, atol=TOL_ABS, rtol=TOL_ROW_REL):
+    """Diagnostic only: share of elements within elementwise allclose(atol, rtol)."""
+    if rows is not None:
+        o, ro = o[rows], ro[rows]
+    if o.size == 0:
+        return 1.0
+    return float(np.mean(np.abs(o - ro) <= atol + rtol * np.abs(ro)))
+
+
 def assert_parity(o, lse, ro, rl, rows=None, label=""):
     ea, er, el = errors(o, lse, ro, rl, rows)
-    say(f"[parity] {label}: max_abs={ea:.3e} max_row_rel={er:.3e} max_lse={el:.3e}")
+    say(f"[parity] {label}: max_abs={ea:.3e} max_row_rel={er:.3e} max_lse={el:.3e} "
+        f"allclose={allclose_fraction(o, ro, rows):.6f}")
     assert ea <= TOL_ABS, f"{label}: max abs error {ea} > {TOL_ABS}"
     assert er <= TOL_ROW_REL, f"{label}: row-relative error {er} > {TOL_ROW_REL}"
     assert el <= TOL_LSE, f"{label}: lse error {el} > {TOL_LSE}"

@@ -269,3 +269,49 @@ def test_recompute_prefill_full_length_sampled():
             ro, rl = attend(bf16_bits_to_f64(b.q[r, h])[None], bf16_bits_to_f64(k_all[:r + 1, g]),
                             bf16_bits_to_f64(v_all[:r + 1, g]), b.scale)
             H.assert_parity(o[r, h][None], lse[r, h][None], ro, rl, label=f"prefill row {r} head {h}")
+
+
+def test_one_plan_shared_by_two_threads_and_streams():
+    """Calls on two streams from two host threads share one plan (distinct workspaces and
+    outputs): every result equals the single-stream one bit for bit."""
+    import threading
+    H.say("[case] plan shared by two threads / streams")
+    b = wl.custom_batch([3000, 17, 900, 5000], num_q_heads=32, num_kv_heads=8, seed=21)
+    cache = H.DeviceCache(b)
+    plan = libra.libra_splitkv_plan(libra.LIBRA_MODE_DECODE, 4, 32, 8, b.seq_lens.tolist(), None,
+                                    num_cus=64)
+    q = H.u16_to_dev(b.q)
+    ref = torch.empty((4, 32, 128), dtype=torch.int16, device="cuda")
+    ws0 = libra.alloc_workspace(plan)
+    libra.libra_decode_attn(cache.layout, plan, q, cache.bt, cache.bt_stride, 4, 32, b.scale, ws0,
+                            ref)
+    torch.cuda.synchronize()
+    results, errors = {}, []
+
+    def worker(t):
+        try:
+            stream = torch.cuda.Stream()
+            ws = libra.alloc_workspace(plan)
+            outs = [torch.empty_like(ref) for _ in range(10)]
+            with torch.cuda.stream(stream):
+                for o in outs:
+                    libra.libra_decode_attn(cache.layout, plan, q, cache.bt, cache.bt_stride, 4,
+                                            32, b.scale, ws, o, stream=stream)
+            stream.synchronize()
+            results[t] = outs
+        except Exception as e:  # reported below
+            errors.append(e)
+
+    threads = [threading.Thread(target=worker, args=(t,)) for t in range(2)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    torch.cuda.synchronize()
+    assert not errors, errors
+    r = H.dev_to_u16(ref)
+    for outs in results.values():
+        for o in outs:
+            assert np.array_equal(H.dev_to_u16(o), r)
+    libra.libra_plan_destroy(plan)
+    cache.close()
