@@ -6,9 +6,9 @@
 // owns 2 column blocks, so a workgroup covers up to 16 * tpb tokens.  Keys are visited
 // 64 at a time: the step's eight 4 KiB tiles (K and V of 4 pages) are loaded into
 // registers two steps ahead, staged in LDS (three stages) and shared by the 8 waves; V
-// is interleaved by page pair on the way
-// in so that each PV operand is a single 16-byte LDS read.  Each wave computes the
-// next step's scores while it turns the current step's into probabilities.  Per page and column block:
+// is interleaved by page pair on the way in so that each PV operand is a single 16-byte
+// LDS read.  Each wave computes the next step's scores while it turns the current
+// step's into probabilities.  Per page and column block:
 //   S^T = K . Q^T (4 mfma 16x16x32), and per page pair O^T += V^T . P^T (8 mfma 16x16x32
 //   over 32 keys).
 // Softmax runs online in base 2.  The running maximum is only moved (and the
