@@ -134,3 +134,35 @@ def test_more_gpus_never_hurt_with_tp1():
         ms, _, _ = rollout_dp_ref(ls, g, [1, 2, 4, 8], MODEL)
         assert ms <= prev + 1e-15
         prev = ms
+
+
+def _partitions(n):
+    """Number of integer partitions of n, by the textbook recurrence over the largest part."""
+    table = [1] + [0] * n
+    for part in range(1, n + 1):
+        for total in range(part, n + 1):
+            table[total] += table[total - part]
+    return table[n]
+
+
+def _tp_multisets(n, degrees=(1, 2, 4, 8)):
+    """Number of ways to split n GPUs into instances of the given TP degrees (as multisets)."""
+    table = [1] + [0] * n
+    for d in degrees:
+        for total in range(d, n + 1):
+            table[total] += table[total - d]
+    return table[n]
+
+
+def test_partition_count_matches_the_paper():
+    """Golden value: Sec. 4.2 prints p(64) ~ 1.7e6 for the search space RolloutDP avoids."""
+    import os
+    path = os.path.join(os.path.dirname(__file__), "golden", "partition_count.txt")
+    rows = [line.split() for line in open(path) if line.strip() and not line.startswith("#")]
+    for n, printed, rtol in rows:
+        assert abs(_partitions(int(n)) - float(printed)) <= float(rtol) * float(printed)
+    assert _partitions(5) == 7 and _partitions(10) == 42          # textbook values
+    # with TP degrees restricted to {1, 2, 4, 8} the instance multisets are far fewer, and
+    # RolloutDP also chooses the contiguous request runs; its brute-force pins above
+    # enumerate both
+    assert _tp_multisets(8) == 10 and _tp_multisets(64) < _partitions(64) / 1000
