@@ -242,8 +242,8 @@ libra_status libra_splitkv_plan(const libra_plan_desc* desc, const int32_t* seq_
 /* Host view of the unit table (valid until libra_plan_destroy). */
 libra_status libra_plan_get_units(libra_plan plan, const int32_t** units_host, int32_t* n_units);
 libra_status libra_plan_get_info(libra_plan plan, libra_plan_info* info);
-/* Bytes of device workspace the plan's calls need (unit, write and merge tables and the
- * float32 partial results of split rows). */
+/* Bytes of device workspace the plan's calls need (unit, write, merge and XCD-queue tables
+ * and the float32 partial results of split rows). */
 size_t libra_plan_workspace_bytes(libra_plan plan);
 /* Copies the plan's tables into `workspace` (device) on `stream`.  Decode / append calls
  * do this themselves when the workspace they get is not the one last uploaded to;

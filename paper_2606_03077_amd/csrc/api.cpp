@@ -149,9 +149,6 @@ libra_status upload(Plan& P, void* ws, size_t ws_bytes, hipStream_t s, bool forc
       e = hipMemcpyAsync(ws, P.pinned, P.upload_bytes, hipMemcpyHostToDevice, s);
       if (e != hipSuccess) return hip_error(e, "hipMemcpyAsync(plan tables)");
     }
-    e = launch_zero_i32(reinterpret_cast<int32_t*>(static_cast<char*>(ws) + P.off_counters),
-                        P.n_counters, s);
-    if (e != hipSuccess) return hip_error(e, "zero counters");
   }
   e = hipEventRecord(P.upload_done, s);
   if (e != hipSuccess) return hip_error(e, "hipEventRecord");

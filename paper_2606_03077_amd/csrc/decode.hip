@@ -36,9 +36,6 @@ constexpr int kThreads = 64 * kWaves;
 #ifndef LIBRA_DECODE_DEPTH
 #define LIBRA_DECODE_DEPTH 2
 #endif
-#ifndef LIBRA_FUSED_MERGE
-#define LIBRA_FUSED_MERGE 0
-#endif
 #ifndef LIBRA_DECODE_WAVES_PER_EU
 #define LIBRA_DECODE_WAVES_PER_EU 3
 #endif
@@ -156,7 +153,6 @@ struct DecodeArgs {
   float* lse;
   float* part_o;
   float* part_lse;
-  int32_t* counters;
   int64_t bt_stride;
   int hkv;
   int hq;
@@ -168,9 +164,6 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(LIBRA_
   __shared__ float red_m[kWaves][16];
   __shared__ float red_l[kWaves][16];
   __shared__ __align__(16) float red_o[kWaves][16][kRedStride];
-#if LIBRA_FUSED_MERGE
-  __shared__ int red_flag;
-#endif
 
   const int32_t* u = A.units + size_t(blockIdx.x) * kUnitInts;
   const int b = u[U_B], g = u[U_G], kv0 = u[U_KV0], kv1 = u[U_KV1];
@@ -305,70 +298,15 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(LIBRA_
     return;
   }
 
-  // Split: store this range's normalised float32 partial and its base-2 log-sum-exp.
-  const size_t slot = size_t(part) + split;
-#if LIBRA_FUSED_MERGE
-  // The last split of a (sequence, KV head) to finish merges all of them.  Partials,
-  // counters and the merge's reads are agent-scope atomics, which the memory model keeps
-  // coherent across XCDs without whole-L2 write-backs or invalidations; s_waitcnt makes
-  // this workgroup's partial stores complete before its counter increment.
-  if (hcol < G) {
-    float* po = A.part_o + (slot * G + hcol) * kDim + c8;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) __hip_atomic_store(po + i, o[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if ((tid & 15) == 0)
-      __hip_atomic_store(A.part_lse + slot * G + hcol, lse2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  int32_t* ctr = A.counters + size_t(b) * A.hkv + g;
-  if (tid == 0) {
-    const int prev = __hip_atomic_fetch_add(ctr, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    red_flag = prev == nsplit - 1;
-  }
-  __syncthreads();
-  if (!red_flag) return;
-  if (hcol < G) {
-    const size_t s0 = size_t(part);
-    float Mg = -INFINITY;
-    for (int j = 0; j < nsplit; ++j)
-      Mg = fmaxf(Mg, __hip_atomic_load(A.part_lse + (s0 + j) * G + hcol, __ATOMIC_RELAXED,
-                                       __HIP_MEMORY_SCOPE_AGENT));
-    float acc8[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    float wsum = 0.f;
-    if (Mg != -INFINITY) {
-      for (int j = 0; j < nsplit; ++j) {
-        const float lj = __hip_atomic_load(A.part_lse + (s0 + j) * G + hcol, __ATOMIC_RELAXED,
-                                           __HIP_MEMORY_SCOPE_AGENT);
-        if (lj == -INFINITY) continue;
-        const float wj = __builtin_amdgcn_exp2f(lj - Mg);
-        wsum += wj;
-        const float* po = A.part_o + ((s0 + j) * G + hcol) * kDim + c8;
-#pragma unroll
-        for (int i = 0; i < 8; ++i)
-          acc8[i] += wj * __hip_atomic_load(po + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      }
-    }
-    const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
-    uint4 ov;
-    ov.x = pack_bf16x2(acc8[0] * inv, acc8[1] * inv);
-    ov.y = pack_bf16x2(acc8[2] * inv, acc8[3] * inv);
-    ov.z = pack_bf16x2(acc8[4] * inv, acc8[5] * inv);
-    ov.w = pack_bf16x2(acc8[6] * inv, acc8[7] * inv);
-    *reinterpret_cast<uint4*>(A.out + (size_t(row) * A.hq + head) * kDim + c8) = ov;
-    if (A.lse && (tid & 15) == 0)
-      A.lse[size_t(row) * A.hq + head] = wsum > 0.f ? (Mg + log2f(wsum)) * kLn2 : -INFINITY;
-  }
-  if (tid == 0) __hip_atomic_store(ctr, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-#else
+  // Split: store this range's normalised float32 partial and its base-2 log-sum-exp;
   // merge_kernel combines the splits after this launch.
+  const size_t slot = size_t(part) + split;
   if (hcol < G) {
     float* po = A.part_o + (slot * G + hcol) * kDim + c8;
     *reinterpret_cast<f32x4*>(po) = f32x4{o[0], o[1], o[2], o[3]};
     *reinterpret_cast<f32x4*>(po + 4) = f32x4{o[4], o[5], o[6], o[7]};
     if ((tid & 15) == 0) A.part_lse[slot * G + hcol] = lse2;
   }
-#endif
 }
 
 struct MergeArgs {
@@ -461,7 +399,6 @@ hipError_t launch_decode(const KvLayout& L, const Plan& P, void* ws, const void*
   A.lse = lse;
   A.part_o = reinterpret_cast<float*>(w + P.off_part_o);
   A.part_lse = reinterpret_cast<float*>(w + P.off_part_lse);
-  A.counters = reinterpret_cast<int32_t*>(w + P.off_counters);
   A.bt_stride = stride;
   A.hkv = P.num_kv_heads;
   A.hq = P.num_q_heads;
@@ -475,7 +412,7 @@ hipError_t launch_decode(const KvLayout& L, const Plan& P, void* ws, const void*
 
 namespace libra {
 
-bool merge_launches(const Plan& P) { return P.info.n_merge_groups > 0 && !LIBRA_FUSED_MERGE; }
+bool merge_launches(const Plan& P) { return P.info.n_merge_groups > 0; }
 
 hipError_t launch_merge(const Plan& P, void* ws, void* out, float* lse, hipStream_t s) {
   const int n = P.info.n_merge_groups;

@@ -45,18 +45,16 @@ struct Plan {
   std::vector<int32_t> xcd_map; // (first chunk unit, count) per XCD queue
   int64_t chunk_grid = 0;       // workgroups of the chunk launch: kNumXcds * longest queue
 
-  // Workspace image: [units | writes | merges | xcd map | counters | partial o | partial lse],
-  // 256-B aligned.  Counters (one per sequence x KV head when any row is split) start at
-  // zero after an upload and are returned to zero by the split merge.
-  size_t off_units = 0, off_writes = 0, off_merges = 0, off_xcd_map = 0, off_counters = 0,
-         off_part_o = 0, off_part_lse = 0;
-  int32_t n_counters = 0;
+  // Workspace image: [units | writes | merges | xcd map | partial o | partial lse],
+  // 256-B aligned.
+  size_t off_units = 0, off_writes = 0, off_merges = 0, off_xcd_map = 0, off_part_o = 0,
+         off_part_lse = 0;
   size_t ws_bytes = 0;
-  size_t upload_bytes = 0;  // bytes of [units | writes | merges] copied from the host
+  size_t upload_bytes = 0;  // bytes of [units | writes | merges | xcd map] from the host
 
   // Upload state (guarded by upload_mu: calls on one plan may come from several threads).
   std::mutex upload_mu;
-  void* pinned = nullptr;         // host staging copy of [units | writes | merges]
+  void* pinned = nullptr;         // host staging copy of [units | writes | merges | xcd map]
   hipEvent_t upload_done = nullptr;
   void* uploaded_ws = nullptr;
 };
@@ -88,7 +86,6 @@ hipError_t launch_decode(const KvLayout& L, const Plan& P, void* ws, const void*
 // Page-run copies (to_run: cache -> packed run; else packed run -> cache).
 hipError_t launch_page_copy(const KvLayout& L, const int32_t* ids, int64_t n, void* k_run,
                             void* v_run, bool to_run, hipStream_t s);
-hipError_t launch_zero_i32(int32_t* p, int64_t n, hipStream_t s);
 hipError_t launch_merge(const Plan& P, void* ws, void* out, float* lse, hipStream_t s);
 bool merge_launches(const Plan& P);  // whether launch_merge enqueues a kernel for P
 hipError_t launch_chunk(const KvLayout& L, const Plan& P, void* ws, const void* q,

@@ -168,20 +168,7 @@ __global__ __launch_bounds__(kThreads) void page_copy_kernel(uint4* __restrict__
   }
 }
 
-// Clears the split-merge counters (a kernel rather than a memset, so that the upload
-// can be captured in a HIP graph).
-__global__ void zero_i32_kernel(int32_t* p, int64_t n) {
-  const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (i < n) p[i] = 0;
-}
-
 }  // namespace
-
-hipError_t launch_zero_i32(int32_t* p, int64_t n, hipStream_t s) {
-  if (n == 0) return hipSuccess;
-  hipLaunchKernelGGL(zero_i32_kernel, dim3(unsigned((n + 255) / 256)), dim3(256), 0, s, p, n);
-  return hipGetLastError();
-}
 
 hipError_t launch_pack(const KvLayout& L, const void* k_src, const void* v_src, int64_t first,
                        int64_t n, hipStream_t s) {

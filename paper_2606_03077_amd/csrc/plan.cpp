@@ -228,9 +228,6 @@ libra_status build_plan(const libra_plan_desc& d, const int32_t* seq_lens, const
   P.off_xcd_map = off;
   off = align256(off + P.xcd_map.size() * sizeof(int32_t));
   P.upload_bytes = off;
-  P.n_counters = slots > 0 ? int32_t(B * Hkv) : 0;
-  P.off_counters = off;
-  off = align256(off + size_t(P.n_counters) * sizeof(int32_t));
   P.off_part_o = off;
   off = align256(off + size_t(slots) * size_t(G) * kDim * sizeof(float));
   P.off_part_lse = off;

@@ -8,7 +8,6 @@ hipError_t launch_unpack(const KvLayout&, void*, void*, int64_t, int64_t, hipStr
 hipError_t launch_gather(const KvLayout&, const int32_t*, int32_t, const int32_t*, int32_t, int32_t, void*, void*, hipStream_t) { return hipErrorUnknown; }
 hipError_t launch_cache_write(const KvLayout&, const Plan&, const void*, const void*, const void*, const int32_t*, int32_t, hipStream_t) { return hipErrorUnknown; }
 hipError_t launch_decode(const KvLayout&, const Plan&, void*, const void*, const int32_t*, int32_t, float, void*, float*, hipStream_t) { return hipErrorUnknown; }
-hipError_t launch_zero_i32(int32_t*, int64_t, hipStream_t) { return hipErrorUnknown; }
 hipError_t launch_merge(const Plan&, void*, void*, float*, hipStream_t) { return hipErrorUnknown; }
 bool merge_launches(const Plan&) { return false; }
 hipError_t launch_chunk(const KvLayout&, const Plan&, void*, const void*, const int32_t*, int32_t, float, void*, float*, hipStream_t) { return hipErrorUnknown; }

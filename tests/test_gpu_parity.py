@@ -200,7 +200,7 @@ def test_append_full_config_sampled():
 def test_split_merge_sees_fresh_partials_when_workspace_is_reused():
     """Same lengths, different values, one plan and one workspace: every call must merge
     its own partials (stale ones from the previous call would go unnoticed with equal
-    inputs), and the merge counters must return to zero after each call."""
+    inputs)."""
     lens = [3000, 17, 5000, 129, 2048]
     H.say(f"[case] workspace reuse lens={lens}")
     batches = [wl.custom_batch(lens, num_q_heads=28, num_kv_heads=4, seed=s) for s in (21, 22, 23)]
