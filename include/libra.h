@@ -59,6 +59,8 @@ enum {
   LIBRA_PAGE_SIZE = 16,     /* tokens per page */
   LIBRA_HEAD_DIM = 128,     /* channels per head */
   LIBRA_MAX_GROUP = 16,     /* largest supported num_q_heads / num_kv_heads */
+  LIBRA_MAX_KV_HEADS = 1024, /* largest supported num_kv_heads (a page's K or V, all heads,
+                                stays under 4 GiB of byte offsets) */
   LIBRA_UNIT_INTS = 12      /* int32 fields per plan unit */
 };
 
@@ -99,7 +101,7 @@ const char* libra_last_error(void);
 typedef struct libra_kv_layout_desc {
   int64_t num_pages;     /* pages in each of k_cache / v_cache, > 0 */
   int32_t page_size;     /* must be LIBRA_PAGE_SIZE */
-  int32_t num_kv_heads;  /* > 0 */
+  int32_t num_kv_heads;  /* in [1, LIBRA_MAX_KV_HEADS] */
   int32_t head_dim;      /* must be LIBRA_HEAD_DIM */
   int32_t dtype;         /* must be LIBRA_DTYPE_BF16 */
   void* k_cache;         /* device, num_pages * num_kv_heads * 4096 bytes */

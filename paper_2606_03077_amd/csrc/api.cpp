@@ -89,6 +89,8 @@ libra_status check_layout(const libra_kv_layout_desc* d) {
   if (d->head_dim != kDim) return set_error(LIBRA_E_UNSUPPORTED, "head_dim must be 128");
   if (d->dtype != LIBRA_DTYPE_BF16) return set_error(LIBRA_E_UNSUPPORTED, "dtype must be bf16");
   if (d->num_kv_heads <= 0) return set_error(LIBRA_E_INVAL, "num_kv_heads must be > 0");
+  if (d->num_kv_heads > LIBRA_MAX_KV_HEADS)
+    return set_error(LIBRA_E_UNSUPPORTED, "num_kv_heads must be <= 1024");
   if (d->num_pages <= 0) return set_error(LIBRA_E_INVAL, "num_pages must be > 0");
   if (d->num_pages > (int64_t(1) << 40) / d->num_kv_heads)
     return set_error(LIBRA_E_INVAL, "num_pages * num_kv_heads too large");

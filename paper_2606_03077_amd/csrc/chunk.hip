@@ -7,8 +7,10 @@
 // 64 at a time: the step's eight 4 KiB tiles (K and V of 4 pages) are loaded into
 // registers two steps ahead, staged in LDS (three stages) and shared by the 8 waves; V
 // is interleaved by page pair on the way in so that each PV operand is a single 16-byte
-// LDS read.  Each wave computes the next step's scores while it turns the current
-// step's into probabilities.  Per page and column block:
+// LDS read.  Each wave works through a step by page pairs: the pair's probabilities,
+// the next step's scores of the same two pages (written over the ones just consumed, so
+// one score set suffices) and the pair's PV, which lets exps overlap score and PV
+// MFMAs.  Per page and column block:
 //   S^T = K . Q^T (4 mfma 16x16x32), and per page pair O^T += V^T . P^T (8 mfma 16x16x32
 //   over 32 keys).
 // Softmax runs online in base 2.  The running maximum is only moved (and the
@@ -121,12 +123,16 @@ void chunk_kernel(ChunkArgs A) {
   const int npages = (kv1 + kPage - 1) / kPage;
   const int nsteps = (npages + kStepPages - 1) / kStepPages;
   const int32_t* btrow = A.bt + int64_t(b) * A.bt_stride;
-  const size_t head_off = size_t(g) * kTileElems;
-  const size_t page_stride = size_t(A.hkv) * kTileElems;
   const int half = tid >> 8;          // 0: this thread stages K tiles, 1: V tiles
   const int elem = tid & 255;         // uint4 index inside a tile
-  const uint16_t* src_cache = half ? A.v_cache : A.k_cache;
+  // This thread's 16 bytes of tile (page 0, head g); page p adds p * page_bytes (one
+  // 32 x 32 -> 64-bit multiply-add per load; num_kv_heads <= 1024 keeps it in 32 bits).
+  const char* lane_base = reinterpret_cast<const char*>(half ? A.v_cache : A.k_cache) +
+                          size_t(g) * kTileBytes + size_t(elem) * 16;
+  const uint32_t page_bytes = uint32_t(A.hkv) * kTileBytes;
   const int first_tok = prior + q0;   // smallest query position of the tile
+  // Steps whose first key is past this need the causal / length mask.
+  const int mask_key0 = min(first_tok - (kStepPages * kPage - 1), kv1 - kStepPages * kPage);
 
   // Thread t stages uint4 `elem` of the K (t < 256) or V tile of each page of a step.
   // The step's 4 page ids come from LDS in one broadcast read; pages past the end
@@ -147,10 +153,8 @@ void chunk_kernel(ChunkArgs A) {
         ids[j] = __builtin_amdgcn_readfirstlane(btrow[min(p0 + j, npages - 1)]);
     }
 #pragma unroll
-    for (int j = 0; j < kStepPages; ++j) {
-      const size_t base = size_t(ids[j]) * page_stride + head_off;
-      r[j] = reinterpret_cast<const uint4*>(src_cache + base)[elem];
-    }
+    for (int j = 0; j < kStepPages; ++j)
+      r[j] = *reinterpret_cast<const uint4*>(lane_base + uint64_t(uint32_t(ids[j])) * page_bytes);
   };
   auto stash = [&](int buf, const uint4 (&r)[kStepPages]) {
     if (half == 0) {
@@ -172,28 +176,24 @@ void chunk_kernel(ChunkArgs A) {
   for (int i = tid; i < nids; i += kThreads) lds_ids[i] = btrow[min(i, npages - 1)];
   __syncthreads();
 
-  // Scores S^T = K . Q^T of one step's 4 pages for both column blocks.
-  auto qk = [&](int buf, f32x4 (&s)[kStepPages][kNB]) {
+  // Scores S^T = K . Q^T of page j of a stage, both column blocks.
+  auto qk_page = [&](int buf, int j, f32x4 (&sj)[kNB]) {
+    uint4 kr[4];
 #pragma unroll
-    for (int j = 0; j < kStepPages; ++j) {
-      uint4 kr[4];
+    for (int i = 0; i < 4; ++i) kr[i] = ldk[buf][j][i * 64 + lane];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) kr[i] = ldk[buf][j][i * 64 + lane];
+    for (int nb = 0; nb < kNB; ++nb) {
+      f32x4 a = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int nb = 0; nb < kNB; ++nb) {
-        f32x4 a = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int i = 0; i < 4; ++i) a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kr[i]), qop[nb][i], a, 0, 0, 0);
-        s[j][nb] = a;
-      }
+      for (int i = 0; i < 4; ++i) a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kr[i]), qop[nb][i], a, 0, 0, 0);
+      sj[nb] = a;
     }
   };
 
   // Step n's causal mask and running-maximum update (small, with branches): gives the
   // exponent offset -m of each column block.
   auto prepare = [&](int key0, f32x4 (&s)[kStepPages][kNB], float (&neg_m)[kNB]) {
-    const bool masked = key0 + kStepPages * kPage - 1 > first_tok || key0 + kStepPages * kPage > kv1;
-    if (masked) {
+    if (key0 > mask_key0) {
 #pragma unroll
       for (int nb = 0; nb < kNB; ++nb)
 #pragma unroll
@@ -224,73 +224,66 @@ void chunk_kernel(ChunkArgs A) {
     }
   };
 
-  // Branch-free: step n's probabilities (exp2, row sums as a shallow tree, bf16 packing)
-  // and step n + 1's score MFMAs, which do not depend on them; the compiler's own
-  // schedule interleaves the two (explicit scheduling groups measured slower).
-  auto exp_and_next_qk = [&](int nbuf, const f32x4 (&s)[kStepPages][kNB],
-                             const float (&neg_m)[kNB], bf16x8 (&pop)[kNB][2],
-                             f32x4 (&s_next)[kStepPages][kNB]) {
+  // Page pair h of step n: the probabilities of its two pages (consuming s[2h] and
+  // s[2h + 1]), step n + 1's scores of the same two pages written back into them (from
+  // stage kbuf; skipped on the last step), and O^T += V^T P^T over the pair's 32 keys
+  // from stage vbuf.  Exps of one pair overlap the previous pair's PV and this pair's
+  // score MFMAs.  On the last step, V of slots at or past kv1 (never written, possibly
+  // NaN) is zeroed in the operands.
+  auto pair = [&](int h, int kbuf, int vbuf, int key0, f32x4 (&s)[kStepPages][kNB],
+                  const float (&neg_m)[kNB], auto last_tag) {
+    constexpr bool kLast = decltype(last_tag)::value;
+    bf16x8 pop[kNB];
 #pragma unroll
     for (int nb = 0; nb < kNB; ++nb) {
-      float p[kStepPages][4];
+      float p[2][4];
 #pragma unroll
-      for (int j = 0; j < kStepPages; ++j)
+      for (int jj = 0; jj < 2; ++jj)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) p[j][r] = __builtin_amdgcn_exp2f(fmaf(s[j][nb][r], A.sl2, neg_m[nb]));
-      float pp[kStepPages];
+        for (int r = 0; r < 4; ++r)
+          p[jj][r] = __builtin_amdgcn_exp2f(fmaf(s[2 * h + jj][nb][r], A.sl2, neg_m[nb]));
+      l[nb] += ((p[0][0] + p[0][1]) + (p[0][2] + p[0][3])) + ((p[1][0] + p[1][1]) + (p[1][2] + p[1][3]));
+      uint4 pb;
+      pb.x = pack_bf16x2(p[0][0], p[0][1]);
+      pb.y = pack_bf16x2(p[0][2], p[0][3]);
+      pb.z = pack_bf16x2(p[1][0], p[1][1]);
+      pb.w = pack_bf16x2(p[1][2], p[1][3]);
+      pop[nb] = as_bf16x8(pb);
+    }
+    if constexpr (!kLast) {
+      qk_page(kbuf, 2 * h, s[2 * h]);
+      qk_page(kbuf, 2 * h + 1, s[2 * h + 1]);
+    }
+    uint4 vo[8];
 #pragma unroll
-      for (int j = 0; j < kStepPages; ++j) pp[j] = (p[j][0] + p[j][1]) + (p[j][2] + p[j][3]);
-      l[nb] += (pp[0] + pp[1]) + (pp[2] + pp[3]);
+    for (int db = 0; db < 8; ++db)
+      vo[db] = *reinterpret_cast<const uint4*>(&ldv[vbuf][h][db >> 1][db & 1][lane][0]);
+    if constexpr (kLast) {
+      const int ka = min(max(kv1 - key0 - 2 * h * kPage - 4 * quad, 0), 4);
+      const int kb = min(max(kv1 - key0 - (2 * h + 1) * kPage - 4 * quad, 0), 4);
+      const uint32_t ma0 = ka >= 2 ? ~0u : (ka == 1 ? 0x0000FFFFu : 0u);
+      const uint32_t ma1 = ka >= 4 ? ~0u : (ka == 3 ? 0x0000FFFFu : 0u);
+      const uint32_t mb0 = kb >= 2 ? ~0u : (kb == 1 ? 0x0000FFFFu : 0u);
+      const uint32_t mb1 = kb >= 4 ? ~0u : (kb == 3 ? 0x0000FFFFu : 0u);
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        uint4 pb;
-        pb.x = pack_bf16x2(p[2 * h][0], p[2 * h][1]);
-        pb.y = pack_bf16x2(p[2 * h][2], p[2 * h][3]);
-        pb.z = pack_bf16x2(p[2 * h + 1][0], p[2 * h + 1][1]);
-        pb.w = pack_bf16x2(p[2 * h + 1][2], p[2 * h + 1][3]);
-        pop[nb][h] = as_bf16x8(pb);
+      for (int db = 0; db < 8; ++db) {
+        vo[db].x &= ma0;
+        vo[db].y &= ma1;
+        vo[db].z &= mb0;
+        vo[db].w &= mb1;
       }
     }
-    qk(nbuf, s_next);
-  };
-
-  // O^T += V^T P^T over each page pair (32 keys) of one step.  On the last step, V of
-  // slots at or past kv1 (never written, possibly NaN) is zeroed in the operands.
-  auto pv = [&](int buf, int key0, const bf16x8 (&pop)[kNB][2], auto last_tag) {
-    constexpr bool kLast = decltype(last_tag)::value;
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      uint4 vo[8];
+    for (int db = 0; db < 8; ++db)
 #pragma unroll
-      for (int db = 0; db < 8; ++db)
-        vo[db] = *reinterpret_cast<const uint4*>(&ldv[buf][h][db >> 1][db & 1][lane][0]);
-      if constexpr (kLast) {
-        const int ka = min(max(kv1 - key0 - 2 * h * kPage - 4 * quad, 0), 4);
-        const int kb = min(max(kv1 - key0 - (2 * h + 1) * kPage - 4 * quad, 0), 4);
-        const uint32_t ma0 = ka >= 2 ? ~0u : (ka == 1 ? 0x0000FFFFu : 0u);
-        const uint32_t ma1 = ka >= 4 ? ~0u : (ka == 3 ? 0x0000FFFFu : 0u);
-        const uint32_t mb0 = kb >= 2 ? ~0u : (kb == 1 ? 0x0000FFFFu : 0u);
-        const uint32_t mb1 = kb >= 4 ? ~0u : (kb == 3 ? 0x0000FFFFu : 0u);
-#pragma unroll
-        for (int db = 0; db < 8; ++db) {
-          vo[db].x &= ma0;
-          vo[db].y &= ma1;
-          vo[db].z &= mb0;
-          vo[db].w &= mb1;
-        }
-      }
-#pragma unroll
-      for (int db = 0; db < 8; ++db)
-#pragma unroll
-        for (int nb = 0; nb < kNB; ++nb)
-          acc[nb][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(vo[db]), pop[nb][h], acc[nb][db], 0, 0, 0);
-    }
+      for (int nb = 0; nb < kNB; ++nb)
+        acc[nb][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(vo[db]), pop[nb], acc[nb][db], 0, 0, 0);
   };
 
   // Software pipeline over steps, three LDS stages: while step n's probabilities are
   // formed and multiplied into V, step n + 1's scores are computed from its K (the two
-  // are independent, so matrix and vector work interleave within each wave) and step
-  // n + 2 is in flight from memory.
+  // are independent, so matrix and vector work interleave within each wave) and steps
+  // n + 2 and n + 3 are in flight from memory.
   // Staging registers come in two sets: step n + 3 is loaded into one while step n + 2,
   // loaded a whole step earlier, waits in the other to be written to LDS at the end of
   // step n, so each load has two steps of compute to land.
@@ -309,49 +302,46 @@ void chunk_kernel(ChunkArgs A) {
   __syncthreads();
   if (nsteps > 2) fetch(2, stage_a);
 
-  f32x4 s_a[kStepPages][kNB], s_b[kStepPages][kNB];
-  if (nsteps > 0) qk(0, s_a);
-  // Every step before the last: no V tail to clear, so exp, next scores and PV form one
-  // branch-free block the scheduler can interleave.  `landing` holds step n + 2,
-  // `flying` receives step n + 3; the score and staging sets swap roles every step.
-  using Scores = f32x4[kStepPages][kNB];
+  // One score set: each page's scores are replaced by the next step's as soon as its
+  // probabilities are taken.
+  f32x4 sc[kStepPages][kNB];
+  if (nsteps > 0)
+#pragma unroll
+    for (int j = 0; j < kStepPages; ++j) qk_page(0, j, sc[j]);
+  // Every step before the last: no V tail to clear.  `landing` holds step n + 2,
+  // `flying` receives step n + 3; the staging sets swap roles every step.
   using Stage = uint4[kStepPages];
-  auto step = [&](int n, Scores& s_cur, Scores& s_nxt, Stage& landing, Stage& flying) {
+  // `buf` is n % kBufs, carried rather than recomputed.
+  auto next_buf = [](int buf) { return buf == kBufs - 1 ? 0 : buf + 1; };
+  auto step = [&](int n, int buf, Stage& landing, Stage& flying) {
     const int key0 = n * kStepPages * kPage;
+    const int buf1 = next_buf(buf), buf2 = next_buf(buf1);
     float neg_m[kNB];
-    prepare(key0, s_cur, neg_m);
-    bf16x8 pop[kNB][2];
-    exp_and_next_qk((n + 1) % kBufs, s_cur, neg_m, pop, s_nxt);
+    prepare(key0, sc, neg_m);
+    pair(0, buf1, buf, key0, sc, neg_m, std::false_type{});
     // Unconditional (the last steps re-load the final step's pages, unused), so that the
     // wait before the stash below only ever counts this step's four loads as younger.
     fetch(min(n + 3, nsteps - 1), flying);
-    pv(n % kBufs, key0, pop, std::false_type{});
-    if (n + 2 < nsteps) stash((n + 2) % kBufs, landing);
+    pair(1, buf1, buf, key0, sc, neg_m, std::false_type{});
+    if (n + 2 < nsteps) stash(buf2, landing);
     __syncthreads();
   };
-  int n0 = 0;
+  int n0 = 0, buf0 = 0;
   for (; n0 + 2 < nsteps; n0 += 2) {
-    step(n0, s_a, s_b, stage_a, stage_b);
-    step(n0 + 1, s_b, s_a, stage_b, stage_a);
+    step(n0, buf0, stage_a, stage_b);
+    step(n0 + 1, next_buf(buf0), stage_b, stage_a);
+    buf0 = next_buf(next_buf(buf0));
   }
   if (n0 + 1 < nsteps) {
-    step(n0, s_a, s_b, stage_a, stage_b);
-#pragma unroll
-    for (int j = 0; j < kStepPages; ++j)
-#pragma unroll
-      for (int nb = 0; nb < kNB; ++nb) s_a[j][nb] = s_b[j][nb];
+    step(n0, buf0, stage_a, stage_b);
+    buf0 = next_buf(buf0);
   }
-  Scores& s_cur = s_a;
-  Scores& s_nxt = s_b;
   if (nsteps > 0) {
-    const int n = nsteps - 1;
-    const int key0 = n * kStepPages * kPage;
+    const int key0 = (nsteps - 1) * kStepPages * kPage;
     float neg_m[kNB];
-    prepare(key0, s_cur, neg_m);
-    bf16x8 pop[kNB][2];
-    // The next-score MFMAs read a stale stage here; their result is unused.
-    exp_and_next_qk((n + 1) % kBufs, s_cur, neg_m, pop, s_nxt);
-    pv(n % kBufs, key0, pop, std::true_type{});
+    prepare(key0, sc, neg_m);
+    pair(0, 0, buf0, key0, sc, neg_m, std::true_type{});
+    pair(1, 0, buf0, key0, sc, neg_m, std::true_type{});
   }
 
   // Epilogue: every column is owned by one wave; normalise and store.

@@ -142,6 +142,8 @@ def test_layout_validation_codes():
     assert create(dtype=7) == 2
     assert create(num_pages=0) == 1
     assert create(num_kv_heads=0) == 1
+    assert create(num_kv_heads=1024) == 0
+    assert create(num_kv_heads=1025) == 2
     assert create(k_cache=None) == 1
     assert create(v_cache=fake + 2) == 1  # misaligned
 
