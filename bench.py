@@ -545,7 +545,7 @@ def main():
     ap.add_argument("--migrate-tp", default="1,2",
                     help="migrate workload: source and target TP degree (head shards)")
     ap.add_argument("--flush-mib", type=int, default=1024)
-    ap.add_argument("--units-per-cu", type=int, default=4)
+    ap.add_argument("--units-per-cu", type=int, default=3)
     ap.add_argument("--min-split-pages", type=int, default=16)
     ap.add_argument("--max-splits", type=int, default=64)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -727,7 +727,7 @@ def main():
         "step_ms_p10_p50_p90": [round(p10, 5), round(p50, 5), round(p90, 5)],
         "timed_wall_s": round(wall, 4),
         "plan_ms": round(float(np.median(plan_times)), 4),
-        "plan": dict({k: info[k] for k in ("n_units", "n_single", "n_chunk", "n_partial_slots",
+        "plan": dict({k: info[k] for k in ("n_units", "n_single", "n_chunk", "n_partial_slots", "balanced",
                                            "chunk_pages", "num_cus")}, **plan_kw),
         "algorithmic_bytes": ab["total"],
         "flops": fl,

@@ -183,23 +183,32 @@ libra_status libra_kv_reshard_host(const void* const* src, int32_t n_src, int32_
  *
  * 1. pages_b = ceil(L_b / 16), L_b = KV length after this step's new tokens.
  * 2. Rows with C_b = 1 query token are single rows, rows with C_b > 1 chunk rows.
- * 3. W = sum over single rows of pages_b * Hkv; target = num_cus * units_per_cu;
- *    chunk = max(min_split_pages, ceil(W / target)) (min_split_pages if W = 0).
- * 4. A single row splits into n_b = min(max_splits, max(1, ceil(pages_b / chunk))) KV
- *    ranges; split j covers pages [floor(j pages_b / n_b), floor((j+1) pages_b / n_b)),
- *    i.e. tokens [16 p0, min(16 p1, L_b)).  An empty sequence gets one empty unit.
- * 5. A chunk row is cut into query tiles of T tokens (T = q_tile, or 16 * max(1, 16 / G)
+ * 3. S = num_cus * units_per_cu, meant as one wave of decode workgroups (units_per_cu
+ *    = workgroups resident per compute unit); R = floor(S / Hkv).
+ * 4. One-wave apportionment: if there are at most R single rows, each starts with
+ *    n_b = 1 and, while sum n_b < R, the single row with the largest pages_b / n_b (exact
+ *    comparison, ties to the smaller b) among those that can still be split (n_b <
+ *    max_splits and pages_b >= (n_b + 1) * min_split_pages) gets one more split; it
+ *    stops early when none can.  This minimises the largest piece, max ceil(pages_b /
+ *    n_b).  The result is used when 2 * (largest piece) * R <= 3 * sum pages_b (at most
+ *    1.5 times the mean share); otherwise, or with more than R single rows, step 5.
+ * 5. Chunk rule: W = sum over single rows of pages_b * Hkv; chunk = max(min_split_pages,
+ *    ceil(W / S)) (min_split_pages if W = 0); n_b = min(max_splits, max(1,
+ *    ceil(pages_b / chunk))).
+ * 6. Split j of a single row covers pages [floor(j pages_b / n_b), floor((j+1) pages_b /
+ *    n_b)), i.e. tokens [16 p0, min(16 p1, L_b)).  An empty sequence gets one empty unit.
+ * 7. A chunk row is cut into query tiles of T tokens (T = q_tile, or 16 * max(1, 16 / G)
  *    if q_tile = 0): tile k holds new tokens [kT, min(kT + T, C_b)) and keys
  *    [0, P_b + min(kT + T, C_b)), P_b = L_b - C_b.  Tiles are not split along KV.
- * 6. Every unit is repeated for each KV head g.
- * 7. Single units come first, by descending KV tokens, ties by ascending (b, g, j).
+ * 8. Every unit is repeated for each KV head g.
+ * 9. Single units come first, by descending KV tokens, ties by ascending (b, g, j).
  *    Chunk units follow, grouped per (b, g) and dealt to 8 per-XCD queues: a tile costs
  *    KV tokens x query tokens, a group the sum of its tiles; groups by descending cost
  *    (ties ascending (b, g)) go to the queue with the least accumulated cost (ties to the
  *    lowest queue); within a group, tiles by descending cost, ties ascending q_begin;
  *    queue 0's tiles are listed first, then queue 1's, ... (the chunk launch runs queue
  *    x's tiles on workgroups w with w % 8 = x, so all tiles of a group share an L2).
- * 8. Single rows with n_b > 1 own n_b float32 partial-result slots per KV head,
+ * 10. Single rows with n_b > 1 own n_b float32 partial-result slots per KV head,
  *    allotted in ascending (b, g): part_base(b, g) = earlier split rows' slots + g n_b.
  *
  * Unit fields (LIBRA_UNIT_INTS int32): b, g, kv_begin, kv_end, q_begin, q_end, split,
@@ -209,7 +218,7 @@ libra_status libra_kv_reshard_host(const void* const* src, int32_t n_src, int32_
  */
 typedef struct libra_plan_params {
   int32_t num_cus;          /* compute units; 0 = query the current device */
-  int32_t units_per_cu;     /* default 4 */
+  int32_t units_per_cu;     /* default 3 (decode workgroups resident per CU) */
   int32_t min_split_pages;  /* default 16 */
   int32_t max_splits;       /* default 64 */
   int32_t q_tile;           /* chunk query tile in tokens; 0 = 16 * max(1, 16 / G) */
@@ -227,12 +236,13 @@ typedef struct libra_plan_info {
   int32_t n_single;         /* units handled by the decode kernel */
   int32_t n_chunk;          /* units handled by the chunk kernel */
   int32_t n_partial_slots;  /* float32 partial results used by split rows */
-  int64_t chunk_pages;      /* step 3's chunk size */
-  int32_t q_tile;           /* step 5's tile size */
+  int64_t chunk_pages;      /* step 5's chunk size (computed even when step 4 decides) */
+  int32_t q_tile;           /* step 7's tile size */
   int32_t n_rows;           /* query rows (sum C_b) */
   int32_t n_write_tiles;    /* (sequence, page) pairs an append writes */
   int32_t num_cus;          /* CUs the plan was cut for */
   int32_t n_merge_groups;   /* (sequence, KV head) pairs whose splits are merged */
+  int32_t balanced;         /* 1 if step 4 set the split counts, 0 if step 5 did */
 } libra_plan_info;
 
 /* Builds the plan from host lengths.  seq_lens_host: int32 [batch], L_b >= 0 (>= C_b

@@ -19,24 +19,36 @@ units per CU, minimum split size in pages, maximum splits, chunk query tile).
 
 1. pages_b = ceil(L_b / 16).
 2. Rows with C_b = 1 are *single* rows; rows with C_b > 1 are *chunk* rows.
-3. W = sum over single rows of pages_b * Hkv; target = num_cus * units_per_cu;
-   chunk = max(min_split_pages, ceil(W / target)) (min_split_pages when W = 0).
-4. A single row is cut into n_b = min(max_splits, max(1, ceil(pages_b / chunk))) splits;
-   split j covers pages [floor(j pages_b / n_b), floor((j+1) pages_b / n_b)), i.e. tokens
-   [16 p0, min(16 p1, L_b)).  An empty sequence gets one empty unit.
-5. A chunk row is cut into query tiles of T tokens (T = q_tile, or 16 * max(1, 16 // G)
+3. S = num_cus * units_per_cu (units_per_cu is meant to be the number of decode
+   workgroups that are resident on one compute unit at a time, so that S units form a
+   single wave); R = floor(S / Hkv) split budget per KV head.
+4. One-wave apportionment.  If the number of single rows is at most R, every single row
+   starts with n_b = 1 split, and while sum n_b < R one more split goes to the single row
+   with the largest pages_b / n_b (compared exactly, ties to the smallest b) among the
+   rows that can still be split: n_b < max_splits and pages_b >= (n_b + 1) *
+   min_split_pages.  It stops early when no row can be split.  This gives the smallest
+   possible largest piece, max ceil(pages_b / n_b), for that many splits.  The result is
+   kept when it is balanced, 2 * max_b ceil(pages_b / n_b) * R <= 3 * sum_b pages_b (the
+   largest piece at most 1.5 times the mean share of a unit); otherwise, and whenever
+   there are more single rows than R, step 5 decides instead.
+5. Chunk rule: W = sum over single rows of pages_b * Hkv; chunk = max(min_split_pages,
+   ceil(W / S)) (min_split_pages when W = 0);
+   n_b = min(max_splits, max(1, ceil(pages_b / chunk))).
+6. Split j of a single row covers pages [floor(j pages_b / n_b), floor((j+1) pages_b /
+   n_b)), i.e. tokens [16 p0, min(16 p1, L_b)).  An empty sequence gets one empty unit.
+7. A chunk row is cut into query tiles of T tokens (T = q_tile, or 16 * max(1, 16 // G)
    when q_tile = 0): tile k holds new tokens [kT, min(kT + T, C_b)) and keys
    [0, P_b + min(kT + T, C_b)), where P_b = L_b - C_b.  Tiles are not split along KV.
-6. Every unit is repeated for each KV head g.
-7. Single units are ordered by descending KV token count, ties by ascending (b, g, j).
+8. Every unit is repeated for each KV head g.
+9. Single units are ordered by descending KV token count, ties by ascending (b, g, j).
    Chunk units are grouped per (b, g); a tile costs KV tokens x query tokens and a group
    the sum of its tiles.  Groups, by descending cost (ties ascending (b, g)), are dealt to
    8 queues (one per XCD), each to the queue with the least accumulated cost (ties to the
    lowest queue).  Within a group, tiles go by descending cost, ties ascending q_begin.
    The table lists all single units, then queue 0's tiles, queue 1's, ... queue 7's.
-8. Single rows with n_b > 1 own n_b partial-result slots per KV head, allotted in
-   ascending (b, g) order: part_base(b, g) = (slots of earlier split rows) + g * n_b.
-   Units with n_b = 1 have part_base = -1.
+10. Single rows with n_b > 1 own n_b partial-result slots per KV head, allotted in
+    ascending (b, g) order: part_base(b, g) = (slots of earlier split rows) + g * n_b.
+    Units with n_b = 1 have part_base = -1.
 
 Each unit is 12 int32 fields, in the order of ``UNIT_FIELDS``.
 """
@@ -55,7 +67,7 @@ NUM_XCDS = 8
 @dataclasses.dataclass(frozen=True)
 class PlanParams:
     num_cus: int = 256
-    units_per_cu: int = 4
+    units_per_cu: int = 3
     min_split_pages: int = 16
     max_splits: int = 64
     q_tile: int = 0
@@ -63,6 +75,38 @@ class PlanParams:
 
 def _ceil_div(a: int, b: int) -> int:
     return -(-a // b)
+
+
+def _apportion(pages, single, R, params):
+    """Step 4's greedy: split counts n_b (sum at most R) of the single rows."""
+    n = {b: 1 for b in single}
+    total = len(single)
+
+    def can_split(b):
+        return n[b] < params.max_splits and pages[b] >= (n[b] + 1) * params.min_split_pages
+
+    while total < R:
+        best = None
+        for b in single:   # ascending b, replaced only on a strictly larger share
+            if can_split(b) and (best is None or pages[b] * n[best] > pages[best] * n[b]):
+                best = b
+        if best is None:
+            break
+        n[best] += 1
+        total += 1
+    return n
+
+
+def _one_wave_splits(pages, single, R, params):
+    """Step 4: split counts of the single rows for one wave of R units per KV head, or
+    None when there are no single rows, they do not fit, or the result is unbalanced."""
+    if not single or len(single) > R:
+        return None
+    n = _apportion(pages, single, R, params)
+    largest = max(_ceil_div(pages[b], n[b]) for b in single)
+    if 2 * largest * R > 3 * sum(pages[b] for b in single):
+        return None
+    return n
 
 
 def plan_ref(seq_lens, q_lens, num_kv_heads: int, group: int, params: PlanParams):
@@ -81,12 +125,16 @@ def plan_ref(seq_lens, q_lens, num_kv_heads: int, group: int, params: PlanParams
     single = [b for b in range(B) if C[b] == 1]
     chunked = [b for b in range(B) if C[b] > 1]
 
+    S = params.num_cus * params.units_per_cu
+    R = S // Hkv
+    n_split = _one_wave_splits(pages, single, R, params)
+    balanced = n_split is not None
     W = sum(pages[b] * Hkv for b in single)
-    target = params.num_cus * params.units_per_cu
-    chunk = max(params.min_split_pages, _ceil_div(W, target)) if W > 0 else params.min_split_pages
-    n_split = {}
-    for b in single:
-        n_split[b] = min(params.max_splits, max(1, _ceil_div(pages[b], chunk)))
+    chunk = max(params.min_split_pages, _ceil_div(W, S)) if W > 0 else params.min_split_pages
+    if not balanced:
+        n_split = {}
+        for b in single:
+            n_split[b] = min(params.max_splits, max(1, _ceil_div(pages[b], chunk)))
 
     part_base = {}
     slots = 0
@@ -134,6 +182,6 @@ def plan_ref(seq_lens, q_lens, num_kv_heads: int, group: int, params: PlanParams
     chunks = [u for q in queues for u in q]
 
     info = {"n_single": len(singles), "n_chunk": len(chunks), "n_partial_slots": slots,
-            "chunk_pages": chunk, "q_tile": T, "work_pages": W,
+            "chunk_pages": chunk, "q_tile": T, "work_pages": W, "balanced": balanced,
             "xcd_queue_lens": [len(q) for q in queues]}
     return singles + chunks, info

@@ -373,7 +373,7 @@ libra_status libra_splitkv_plan(const libra_plan_desc* desc, const int32_t* seq_
   if (d.mode == LIBRA_MODE_APPEND && d.batch > 0 && !q_lens_host)
     return set_error(LIBRA_E_INVAL, "append plans need q_lens_host");
 
-  libra_plan_params p{0, 4, 16, 64, 0};
+  libra_plan_params p{0, 3, 16, 64, 0};
   if (params) p = *params;
   if (p.num_cus == 0) {
     int dev = 0, cus = 0;

@@ -2,6 +2,7 @@
 #include <algorithm>
 #include <array>
 #include <cstring>
+#include <queue>
 
 #include "internal.h"
 
@@ -12,6 +13,42 @@ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 using Unit = std::array<int32_t, kUnitInts>;
+
+// Rule step 4: split counts that cut the single rows into at most R pieces per KV head
+// with the smallest possible largest piece.  Each extra split goes to the row with the
+// largest share pages_b / n_b (exact cross-multiplied comparison, ties to the smaller b)
+// among the rows that can still be split; a row that cannot be split now never can, as
+// only its own split count would change that.  Returns false (nsplit untouched) when the
+// rows do not fit in R or the largest piece exceeds 1.5 times the mean share.
+bool one_wave_splits(const std::vector<int64_t>& pages, const std::vector<int64_t>& single,
+                     int64_t R, const libra_plan_params& p, std::vector<int64_t>& nsplit) {
+  if (single.empty() || int64_t(single.size()) > R) return false;
+  std::vector<int64_t> n(pages.size(), 1);
+  auto before = [&](int64_t a, int64_t b) {  // true if row a's share is served after b's
+    const int64_t lhs = pages[a] * n[b], rhs = pages[b] * n[a];
+    if (lhs != rhs) return lhs < rhs;
+    return a > b;
+  };
+  std::priority_queue<int64_t, std::vector<int64_t>, decltype(before)> heap(before);
+  for (int64_t b : single) heap.push(b);
+  int64_t total = int64_t(single.size());
+  while (total < R && !heap.empty()) {
+    const int64_t b = heap.top();
+    heap.pop();
+    if (n[b] >= p.max_splits || pages[b] < (n[b] + 1) * int64_t(p.min_split_pages)) continue;
+    ++n[b];
+    ++total;
+    heap.push(b);
+  }
+  int64_t largest = 0, sum = 0;
+  for (int64_t b : single) {
+    largest = std::max(largest, ceil_div(pages[b], n[b]));
+    sum += pages[b];
+  }
+  if (__int128(2) * largest * R > __int128(3) * sum) return false;
+  for (int64_t b : single) nsplit[b] = n[b];
+  return true;
+}
 
 }  // namespace
 
@@ -36,20 +73,27 @@ libra_status build_plan(const libra_plan_desc& d, const int32_t* seq_lens, const
   }
   if (rows > INT32_MAX) return set_error(LIBRA_E_INVAL, "too many query rows");
 
-  // Step 3: chunk size from the single rows' total work.
+  // Steps 3-5: one wave of S units per KV head if the single rows can fill it evenly,
+  // else the chunk rule.
+  std::vector<int64_t> single;
   int64_t W = 0;
   for (int64_t b = 0; b < B; ++b)
-    if (C[b] == 1) W += pages[b] * Hkv;
-  const int64_t target = int64_t(p.num_cus) * p.units_per_cu;
-  const int64_t chunk = W > 0 ? std::max<int64_t>(p.min_split_pages, ceil_div(W, target))
+    if (C[b] == 1) {
+      single.push_back(b);
+      W += pages[b] * Hkv;
+    }
+  const int64_t S = int64_t(p.num_cus) * p.units_per_cu;
+  const int64_t chunk = W > 0 ? std::max<int64_t>(p.min_split_pages, ceil_div(W, S))
                               : int64_t(p.min_split_pages);
-
-  // Step 4 + 8: split counts and partial slots in ascending (b, g).
   std::vector<int64_t> nsplit(B, 1), slot_base(B, -1);
+  const bool balanced = one_wave_splits(pages, single, S / Hkv, p, nsplit);
+  if (!balanced)
+    for (int64_t b : single)
+      nsplit[b] = std::min<int64_t>(p.max_splits, std::max<int64_t>(1, ceil_div(pages[b], chunk)));
+
+  // Step 10: partial slots in ascending (b, g).
   int64_t slots = 0;
-  for (int64_t b = 0; b < B; ++b) {
-    if (C[b] != 1) continue;
-    nsplit[b] = std::min<int64_t>(p.max_splits, std::max<int64_t>(1, ceil_div(pages[b], chunk)));
+  for (int64_t b : single) {
     if (nsplit[b] > 1) {
       slot_base[b] = slots;
       slots += nsplit[b] * Hkv;
@@ -89,7 +133,7 @@ libra_status build_plan(const libra_plan_desc& d, const int32_t* seq_lens, const
     return x[U_SPLIT] < y[U_SPLIT];
   });
 
-  // Step 5: query tiles of chunk rows.
+  // Step 7: query tiles of chunk rows.
   const int64_t T = p.q_tile > 0 ? p.q_tile : int64_t(kPage) * std::max<int64_t>(1, 16 / G);
   for (int64_t b = 0; b < B; ++b) {
     if (C[b] == 1) continue;
@@ -114,7 +158,7 @@ libra_status build_plan(const libra_plan_desc& d, const int32_t* seq_lens, const
       }
     }
   }
-  // Step 7 (chunk units): XCD-affine order.  Tiles of one (b, g) read the same keys, so
+  // Step 9 (chunk units): XCD-affine order.  Tiles of one (b, g) read the same keys, so
   // they are kept on one XCD (workgroup w runs on XCD w % kNumXcds) to share its L2.
   // Groups by descending total cost (ties ascending (b, g)) are dealt to the XCD queue
   // with the least accumulated cost (ties to the lowest queue); inside a group, tiles by
@@ -217,6 +261,7 @@ libra_status build_plan(const libra_plan_desc& d, const int32_t* seq_lens, const
   I.n_write_tiles = int32_t(P.writes.size() / kWriteInts);
   I.num_cus = p.num_cus;
   I.n_merge_groups = int32_t(P.merges.size() / kMergeInts);
+  I.balanced = balanced ? 1 : 0;
 
   size_t off = 0;
   P.off_units = off;

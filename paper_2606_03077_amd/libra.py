@@ -71,7 +71,8 @@ class PlanInfo(ctypes.Structure):
                 ("n_chunk", ctypes.c_int32), ("n_partial_slots", ctypes.c_int32),
                 ("chunk_pages", ctypes.c_int64), ("q_tile", ctypes.c_int32),
                 ("n_rows", ctypes.c_int32), ("n_write_tiles", ctypes.c_int32),
-                ("num_cus", ctypes.c_int32), ("n_merge_groups", ctypes.c_int32)]
+                ("num_cus", ctypes.c_int32), ("n_merge_groups", ctypes.c_int32),
+                ("balanced", ctypes.c_int32)]
 
 
 class CePoly(ctypes.Structure):
@@ -280,7 +281,7 @@ def libra_kv_gather(layout: int, block_table, bt_stride: int, cu_seq_lens, batch
 
 def libra_splitkv_plan(mode: int, batch: int, num_q_heads: int, num_kv_heads: int,
                        seq_lens: Sequence[int], q_lens: Optional[Sequence[int]] = None,
-                       num_cus: int = 0, units_per_cu: int = 4, min_split_pages: int = 16,
+                       num_cus: int = 0, units_per_cu: int = 3, min_split_pages: int = 16,
                        max_splits: int = 64, q_tile: int = 0) -> int:
     d = PlanDesc(mode, batch, num_q_heads, num_kv_heads)
     p = PlanParams(num_cus, units_per_cu, min_split_pages, max_splits, q_tile)

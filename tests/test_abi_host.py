@@ -63,6 +63,8 @@ def _compare(lens, qlens, hq, hkv, params):
     assert info["n_single"] == rinfo["n_single"] and info["n_chunk"] == rinfo["n_chunk"]
     assert info["n_partial_slots"] == rinfo["n_partial_slots"]
     assert info["chunk_pages"] == rinfo["chunk_pages"] and info["q_tile"] == rinfo["q_tile"]
+    assert info["balanced"] == int(rinfo["balanced"])
+    return info
 
 
 @pytest.mark.parametrize("name", ["tiny", "7b", "longtail", "straggler", "append"])
@@ -73,6 +75,40 @@ def test_plan_bit_exact_on_workload_lengths(name):
     for params in [oracle.PlanParams(), oracle.PlanParams(num_cus=256, units_per_cu=3,
                                                           min_split_pages=8, max_splits=128)]:
         _compare(lens.tolist(), q, w.num_q_heads, w.num_kv_heads, params)
+
+
+def test_plan_branch_per_workload():
+    # Default parameters on 256 CUs: the 7B-class and straggler batches fit one wave of
+    # 768 units evenly; the long-tailed batch has more rows than a wave, and the append
+    # batch's single rows (96 x 8 KV heads = one wave) cannot be balanced without splits.
+    expect = {"tiny": False, "7b": True, "longtail": False, "straggler": True, "append": False}
+    for name, balanced in expect.items():
+        w = wl.WORKLOADS[name]
+        lens, qlens = wl.draw_lengths(w, np.random.default_rng(w.seed))
+        q = qlens.tolist() if w.append else None
+        info = _compare(lens.tolist(), q, w.num_q_heads, w.num_kv_heads, oracle.PlanParams())
+        assert info["balanced"] == int(balanced), name
+
+
+def _one_wave_case(seed):
+    # Lognormal lengths with a budget that usually admits the one-wave apportionment,
+    # including ties between equal rows and the max_splits / min_split_pages limits.
+    rng = np.random.default_rng(2000 + seed)
+    B = int(rng.integers(1, 120))
+    lens = np.clip(np.rint(np.exp(np.log(2048) + rng.standard_normal(B))), 0, 70000)
+    lens[rng.random(B) < 0.1] = 4096
+    hkv = int(rng.choice([1, 2, 4, 8]))
+    upc = int(rng.integers(1, 5))
+    waves = float(rng.choice([1.0, 1.5, 3.0, 6.0]))   # budget R relative to the row count
+    params = oracle.PlanParams(num_cus=int(np.ceil(waves * B * hkv / upc)), units_per_cu=upc,
+                               min_split_pages=int(rng.choice([1, 4, 16])),
+                               max_splits=int(rng.choice([3, 16, 64, 64])))
+    return _compare(lens.astype(int).tolist(), None, 4 * hkv, hkv, params)["balanced"]
+
+
+def test_plan_bit_exact_one_wave_random():
+    taken = [_one_wave_case(seed) for seed in range(24)]
+    assert 4 <= sum(taken) < len(taken)   # both branches of rule step 4 are exercised
 
 
 @pytest.mark.parametrize("seed", range(12))

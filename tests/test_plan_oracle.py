@@ -149,3 +149,69 @@ def test_straggler_batch_splits_every_row():
     units, info = check_invariants(lens, None, 8, 8, PlanParams())
     assert all(u[F["n_splits"]] >= 8 for u in units)
     assert len(units) >= 256
+
+
+def test_hand_derived_one_wave_apportionment():
+    # L = [160, 48, 1600] -> pages [10, 3, 100]; Hkv = 2, S = 4 * 4 = 16, R = 8.
+    # Three rows fit.  Greedy from n = [1, 1, 1]: row 2's share 100 > 10 > 3 takes splits
+    # until n = [1, 1, 6] (shares 10, 3, 16.7; sum 8 = R).  Largest piece ceil(100/6) = 17
+    # and 2 * 17 * 8 = 272 <= 3 * 113 = 339, so it is kept (the chunk rule would have cut
+    # row 2 into ceil(100 / 15) = 7).  Row 2's pages split at floor(j * 100 / 6) =
+    # 0, 16, 33, 50, 66, 83, 100: tokens 256, 272, 272, 256, 272, 272.
+    units, info = plan_ref([160, 48, 1600], None, 2, 4,
+                           PlanParams(num_cus=4, units_per_cu=4, min_split_pages=2, max_splits=8))
+    cut = [0, 16, 33, 50, 66, 83, 100]
+
+    def u(b, g, j):
+        if b == 2:
+            return (2, g, 16 * cut[j], 16 * cut[j + 1], 0, 1, j, 6, 6 * g, 2, 0, 1599)
+        L = [160, 48][b]
+        return (b, g, 0, L, 0, 1, 0, 1, -1, b, 0, L - 1)
+
+    expect = ([u(2, g, j) for g in (0, 1) for j in (1, 2, 4, 5)]
+              + [u(2, g, j) for g in (0, 1) for j in (0, 3)]
+              + [u(0, 0, 0), u(0, 1, 0), u(1, 0, 0), u(1, 1, 0)])
+    expect = sorted(expect, key=lambda x: (-(x[3] - x[2]), x[0], x[1], x[6]))
+    assert expect[:8] == [u(2, 0, 1), u(2, 0, 2), u(2, 0, 4), u(2, 0, 5),
+                          u(2, 1, 1), u(2, 1, 2), u(2, 1, 4), u(2, 1, 5)]
+    assert units == expect
+    assert info["balanced"] and info["n_partial_slots"] == 12 and info["chunk_pages"] == 15
+
+
+def test_hand_derived_unbalanced_falls_back_to_chunk_rule():
+    # pages [40, 1, 1], Hkv = 1, S = R = 4, min_split 16.  Greedy: n = [2, 1, 1], largest
+    # piece 20, and 2 * 20 * 4 = 160 > 3 * 42 = 126: not balanced.  Chunk rule:
+    # chunk = max(16, ceil(42 / 4)) = 16, n = [ceil(40 / 16), 1, 1] = [3, 1, 1]; row 0's
+    # pages split at floor(j * 40 / 3) = 0, 13, 26, 40.
+    units, info = plan_ref([640, 16, 16], None, 1, 1,
+                           PlanParams(num_cus=1, units_per_cu=4, min_split_pages=16, max_splits=8))
+    assert units == [
+        (0, 0, 416, 640, 0, 1, 2, 3, 0, 0, 0, 639),
+        (0, 0, 0, 208, 0, 1, 0, 3, 0, 0, 0, 639),
+        (0, 0, 208, 416, 0, 1, 1, 3, 0, 0, 0, 639),
+        (1, 0, 0, 16, 0, 1, 0, 1, -1, 1, 0, 15),
+        (2, 0, 0, 16, 0, 1, 0, 1, -1, 2, 0, 15),
+    ]
+    assert not info["balanced"] and info["chunk_pages"] == 16
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_apportionment_is_optimal_by_brute_force(seed):
+    """The greedy attains the smallest possible largest piece over every admissible
+    choice of split counts with the same budget (exhaustive search on tiny inputs)."""
+    import itertools
+    from oracle.plan import _apportion, _ceil_div
+    rng = np.random.default_rng(1000 + seed)
+    B = int(rng.integers(1, 5))
+    pages = [int(x) for x in rng.integers(0, 13, size=B)]
+    params = PlanParams(num_cus=1, units_per_cu=1, min_split_pages=int(rng.integers(1, 4)),
+                        max_splits=int(rng.integers(1, 5)))
+    R = int(rng.integers(B, 3 * B + 3))
+    single = list(range(B))
+    n = _apportion(pages, single, R, params)
+    ub = [max(1, min(params.max_splits, p // params.min_split_pages)) for p in pages]
+    assert all(1 <= n[b] <= ub[b] for b in single)
+    assert sum(n.values()) == min(R, sum(ub))
+    best = min(max(_ceil_div(p, k) for p, k in zip(pages, ks))
+               for ks in itertools.product(*[range(1, u + 1) for u in ub]) if sum(ks) <= R)
+    assert max(_ceil_div(pages[b], n[b]) for b in single) == best
