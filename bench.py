@@ -63,7 +63,7 @@ def flops(batch) -> int:
 
 def kernel_source_sha() -> str:
     h = hashlib.sha256()
-    for f in ("decode.hip", "internal.h"):
+    for f in ("decode.hip", "internal.h", "plan.cpp"):   # the plan sets the partial traffic
         with open(os.path.join(ROOT, "paper_2606_03077_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -72,7 +72,7 @@ def kernel_source_sha() -> str:
 def traffic_from_profile(workload: str):
     """HBM bytes per launch of the decode kernel from committed rocprofv3 counters.
 
-    Null unless profiles/counters.json was taken on the current kernel source.
+    Null unless profiles/counters.json was taken on the current kernel and plan source.
     """
     try:
         with open(PROFILE_COUNTERS) as f:
