@@ -197,17 +197,20 @@ libra_status libra_kv_reshard_host(const void* const* src, int32_t n_src, int32_
  *    ceil(pages_b / chunk))).
  * 6. Split j of a single row covers pages [floor(j pages_b / n_b), floor((j+1) pages_b /
  *    n_b)), i.e. tokens [16 p0, min(16 p1, L_b)).  An empty sequence gets one empty unit.
- * 7. A chunk row is cut into query tiles of T tokens (T = q_tile, or 16 * max(1, 16 / G)
- *    if q_tile = 0): tile k holds new tokens [kT, min(kT + T, C_b)) and keys
+ * 7. A chunk row is cut into query tiles of T tokens (T = q_tile, or floor(256 / G) if
+ *    q_tile = 0): tile k holds new tokens [kT, min(kT + T, C_b)) and keys
  *    [0, P_b + min(kT + T, C_b)), P_b = L_b - C_b.  Tiles are not split along KV.
  * 8. Every unit is repeated for each KV head g.
  * 9. Single units come first, by descending KV tokens, ties by ascending (b, g, j).
  *    Chunk units follow, grouped per (b, g) and dealt to 8 per-XCD queues: a tile costs
- *    KV tokens x query tokens, a group the sum of its tiles; groups by descending cost
- *    (ties ascending (b, g)) go to the queue with the least accumulated cost (ties to the
- *    lowest queue); within a group, tiles by descending cost, ties ascending q_begin;
- *    queue 0's tiles are listed first, then queue 1's, ... (the chunk launch runs queue
- *    x's tiles on workgroups w with w % 8 = x, so all tiles of a group share an L2).
+ *    KV tokens x query tokens, a group the sum of its tiles.  With F = ceil(total / 8), a
+ *    group of cost c and m tiles is cut into n = min(m, ceil(c / F)) parts, tile i
+ *    (ascending q_begin) going to part floor(S_i n / c), S_i = cost of the group's
+ *    earlier tiles; empty parts are dropped.  Parts by descending cost (ties ascending
+ *    (b, g, part)) go to the queue with the least accumulated cost (ties to the lowest
+ *    queue); within a part, tiles by descending cost, ties ascending q_begin; queue 0's
+ *    tiles are listed first, then queue 1's, ... (the chunk launch runs queue x's tiles
+ *    on workgroups w with w % 8 = x, so the tiles of a part share an L2).
  * 10. Single rows with n_b > 1 own n_b float32 partial-result slots per KV head,
  *    allotted in ascending (b, g): part_base(b, g) = earlier split rows' slots + g n_b.
  *
@@ -221,7 +224,7 @@ typedef struct libra_plan_params {
   int32_t units_per_cu;     /* default 3 (decode workgroups resident per CU) */
   int32_t min_split_pages;  /* default 16 */
   int32_t max_splits;       /* default 64 */
-  int32_t q_tile;           /* chunk query tile in tokens; 0 = 16 * max(1, 16 / G) */
+  int32_t q_tile;           /* chunk query tile in tokens, at most floor(256 / G); 0 = that */
 } libra_plan_params;
 
 typedef struct libra_plan_desc {

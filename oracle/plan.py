@@ -36,15 +36,18 @@ units per CU, minimum split size in pages, maximum splits, chunk query tile).
    n_b = min(max_splits, max(1, ceil(pages_b / chunk))).
 6. Split j of a single row covers pages [floor(j pages_b / n_b), floor((j+1) pages_b /
    n_b)), i.e. tokens [16 p0, min(16 p1, L_b)).  An empty sequence gets one empty unit.
-7. A chunk row is cut into query tiles of T tokens (T = q_tile, or 16 * max(1, 16 // G)
-   when q_tile = 0): tile k holds new tokens [kT, min(kT + T, C_b)) and keys
+7. A chunk row is cut into query tiles of T tokens (T = q_tile, or floor(256 / G) when
+   q_tile = 0): tile k holds new tokens [kT, min(kT + T, C_b)) and keys
    [0, P_b + min(kT + T, C_b)), where P_b = L_b - C_b.  Tiles are not split along KV.
 8. Every unit is repeated for each KV head g.
 9. Single units are ordered by descending KV token count, ties by ascending (b, g, j).
    Chunk units are grouped per (b, g); a tile costs KV tokens x query tokens and a group
-   the sum of its tiles.  Groups, by descending cost (ties ascending (b, g)), are dealt to
-   8 queues (one per XCD), each to the queue with the least accumulated cost (ties to the
-   lowest queue).  Within a group, tiles go by descending cost, ties ascending q_begin.
+   the sum of its tiles.  With F = ceil(total cost / 8), a group of cost c and m tiles is
+   cut into n = min(m, ceil(c / F)) parts: its tile i (ascending q_begin) goes to part
+   floor(S_i * n / c), S_i being the cost of the group's tiles before it; empty parts are
+   dropped.  Parts, by descending cost (ties ascending (b, g, part)), are dealt to 8
+   queues (one per XCD), each to the queue with the least accumulated cost (ties to the
+   lowest queue).  Within a part, tiles go by descending cost, ties ascending q_begin.
    The table lists all single units, then queue 0's tiles, queue 1's, ... queue 7's.
 10. Single rows with n_b > 1 own n_b partial-result slots per KV head, allotted in
     ascending (b, g) order: part_base(b, g) = (slots of earlier split rows) + g * n_b.
@@ -157,7 +160,7 @@ def plan_ref(seq_lens, q_lens, num_kv_heads: int, group: int, params: PlanParams
                                 row0[b], KIND_SINGLE, L[b] - 1))
     singles.sort(key=lambda u: (-(u[3] - u[2]), u[0], u[1], u[6]))
 
-    T = params.q_tile if params.q_tile > 0 else PAGE * max(1, 16 // group)
+    T = params.q_tile if params.q_tile > 0 else 256 // group
     chunks = []
     for b in chunked:
         P = L[b] - C[b]
@@ -170,15 +173,24 @@ def plan_ref(seq_lens, q_lens, num_kv_heads: int, group: int, params: PlanParams
         return (u[3] - u[2]) * (u[5] - u[4])
 
     groups = {}
-    for u in chunks:
+    for u in chunks:                      # built in ascending (b, g, q_begin)
         groups.setdefault((u[0], u[1]), []).append(u)
-    order = sorted(groups, key=lambda k: (-sum(cost(u) for u in groups[k]), k[0], k[1]))
+    fair = _ceil_div(sum(cost(u) for u in chunks), NUM_XCDS) if chunks else 1
+    parts = {}
+    for (b, g), tiles in groups.items():
+        c = sum(cost(u) for u in tiles)
+        n = min(len(tiles), _ceil_div(c, fair))
+        before = 0
+        for u in tiles:
+            parts.setdefault((b, g, before * n // c), []).append(u)
+            before += cost(u)
+    order = sorted(parts, key=lambda k: (-sum(cost(u) for u in parts[k]), k))
     queues = [[] for _ in range(NUM_XCDS)]
     qcost = [0] * NUM_XCDS
     for k in order:
         x = min(range(NUM_XCDS), key=lambda i: (qcost[i], i))
-        qcost[x] += sum(cost(u) for u in groups[k])
-        queues[x].extend(sorted(groups[k], key=lambda u: (-cost(u), u[4])))
+        qcost[x] += sum(cost(u) for u in parts[k])
+        queues[x].extend(sorted(parts[k], key=lambda u: (-cost(u), u[4])))
     chunks = [u for q in queues for u in q]
 
     info = {"n_single": len(singles), "n_chunk": len(chunks), "n_partial_slots": slots,

@@ -385,9 +385,8 @@ libra_status libra_splitkv_plan(const libra_plan_desc* desc, const int32_t* seq_
   if (p.num_cus <= 0 || p.units_per_cu <= 0 || p.min_split_pages <= 0 || p.max_splits <= 0 ||
       p.q_tile < 0)
     return set_error(LIBRA_E_INVAL, "plan parameters must be positive");
-  const int tpb = G >= 16 ? 1 : 16 / G;
-  if (p.q_tile > 16 * tpb)
-    return set_error(LIBRA_E_UNSUPPORTED, "q_tile larger than 16 * max(1, 16 / G) tokens");
+  if (p.q_tile > kChunkRows / G)
+    return set_error(LIBRA_E_UNSUPPORTED, "q_tile larger than floor(256 / G) tokens");
 
   auto* P = new (std::nothrow) libra_plan_s();
   if (!P) return set_error(LIBRA_E_NOMEM, "plan allocation failed");

@@ -1,9 +1,10 @@
 // Causal attention of an appended chunk (e.g. a tool output) over the paged KV cache.
 //
 // One 512-thread workgroup (8 waves) per chunk unit (sequence b, KV head g, new tokens
-// [q0, q1)).  Query rows are (token, head) pairs of the G heads sharing KV head g, packed
-// into 16-wide matrix columns, tpb = max(1, 16 / G) tokens per column block; each wave
-// owns 2 column blocks, so a workgroup covers up to 16 * tpb tokens.  Keys are visited
+// [q0, q1)).  Query rows are the (token, head) pairs of the G heads sharing KV head g,
+// token-major, packed 16 to a matrix column block whatever G is (a block may hold the
+// end of one token's heads and the start of the next's); each wave owns 2 column blocks,
+// so a workgroup covers 256 rows, i.e. up to floor(256 / G) tokens.  Keys are visited
 // 64 at a time: the step's eight 4 KiB tiles (K and V of 4 pages) are loaded into
 // registers two steps ahead, staged in LDS (three stages) and shared by the 8 waves; V
 // is interleaved by page pair on the way in so that each PV operand is a single 16-byte
@@ -17,8 +18,9 @@
 // accumulators rescaled) when a step's scores exceed it by more than 2^kTau, which a
 // wave-wide vote detects; otherwise probabilities are taken against the old maximum
 // (at most 2^kTau, exact in the final normalisation).  Causal masks are applied only on
-// steps that reach past the tile's first token.  Column c of block nb in wave w is
-// token q0 + (2 w + nb) * tpb + c / G, head c % G, and sees keys k <= P_b + token.
+// steps that reach past the tile's first token.  Column c of block nb in wave w is row
+// r = 16 (2 w + nb) + c of the tile: token q0 + r / G, head r % G; it sees keys
+// k <= P_b + token.
 // Units arrive in per-XCD queues: workgroup w takes tile w / 8 of queue w % 8, so the
 // tiles of one (b, g), which read the same keys, run on one XCD and share its L2.
 #include <cmath>
@@ -35,6 +37,7 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 constexpr int kWaves = 8;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kNB = 2;           // column blocks per wave
+static_assert(kChunkRows == 16 * kNB * kWaves, "the plan's tile rows are the kernel's");
 constexpr int kStepPages = 4;    // pages (16 keys each) per softmax step
 constexpr float kTau = 8.f;      // lazy-rescale threshold, base-2 logits
 constexpr int kMaxIds = 4096;    // block-table entries staged in LDS (64K keys)
@@ -89,19 +92,19 @@ void chunk_kernel(ChunkArgs A) {
   const int wave = tid >> 6, lane = tid & 63;
   const int col = lane & 15, quad = lane >> 4;
   const int G = A.group;
-  const int tpb = G >= 16 ? 1 : 16 / G;
-  const int head = col % G;
 
-  int tok[kNB], lim[kNB];
+  int tok[kNB], lim[kNB], head[kNB];
   bf16x8 qop[kNB][4];
 #pragma unroll
   for (int nb = 0; nb < kNB; ++nb) {
-    const int t = q0 + (kNB * wave + nb) * tpb + col / G;
-    const bool ok = col < tpb * G && t < q1;
+    const int r = (kNB * wave + nb) * 16 + col;  // row of the tile, token-major
+    const int t = q0 + r / G;
+    head[nb] = r % G;
+    const bool ok = t < q1;
     tok[nb] = ok ? t : -1;
     lim[nb] = ok ? prior + t : -1;  // last visible key position
     const uint4* qrow = reinterpret_cast<const uint4*>(
-        A.q + (size_t(row0 + (ok ? t : 0)) * A.hq + size_t(g) * G + head) * kDim);
+        A.q + (size_t(row0 + (ok ? t : 0)) * A.hq + size_t(g) * G + head[nb]) * kDim);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       uint4 v = make_uint4(0, 0, 0, 0);
@@ -352,7 +355,7 @@ void chunk_kernel(ChunkArgs A) {
     ls += __shfl_xor(ls, 32);
     if (tok[nb] < 0) continue;
     const float inv = ls > 0.f ? 1.f / ls : 0.f;
-    const size_t orow = (size_t(row0 + tok[nb]) * A.hq + size_t(g) * G + head);
+    const size_t orow = (size_t(row0 + tok[nb]) * A.hq + size_t(g) * G + head[nb]);
     uint16_t* op = A.out + orow * kDim + 4 * quad;
 #pragma unroll
     for (int db = 0; db < 8; ++db) {

@@ -25,6 +25,7 @@ enum UnitField : int {
 constexpr int kKindSingle = 0;
 constexpr int kKindChunk = 1;
 constexpr int kNumXcds = 8;  // MI355X: workgroup w is dispatched to XCD w % 8
+constexpr int kChunkRows = 256;  // (token, head) rows of one chunk-kernel tile
 
 // Append cache-write table: one record per (sequence, page) the new tokens touch.
 enum WriteField : int { W_B = 0, W_PAGE, W_SLOT0, W_SLOT1, W_ROW, W_PAD0, W_PAD1, W_PAD2 };

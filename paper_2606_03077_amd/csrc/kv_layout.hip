@@ -126,7 +126,10 @@ __global__ __launch_bounds__(kThreads) void cache_write_kernel(
   const size_t base = tile_elem(page, g, hkv);
   const int t = threadIdx.x;
   const int s = t >> 4, d0 = (t & 15) * 8;
-  *reinterpret_cast<uint4*>(vt + t * 8) = *reinterpret_cast<const uint4*>(v_cache + base + t * 8);
+  // A page whose 16 slots are all new is overwritten whole: its old V tile is not read.
+  // s0 and s1 are uniform over the block, so the barrier below is reached by all threads.
+  if (s1 - s0 < kPage)
+    *reinterpret_cast<uint4*>(vt + t * 8) = *reinterpret_cast<const uint4*>(v_cache + base + t * 8);
   __syncthreads();
   if (s >= s0 && s < s1) {
     const size_t src = (size_t(row + s - s0) * hkv + g) * kDim + d0;

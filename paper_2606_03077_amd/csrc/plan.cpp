@@ -134,7 +134,7 @@ libra_status build_plan(const libra_plan_desc& d, const int32_t* seq_lens, const
   });
 
   // Step 7: query tiles of chunk rows.
-  const int64_t T = p.q_tile > 0 ? p.q_tile : int64_t(kPage) * std::max<int64_t>(1, 16 / G);
+  const int64_t T = p.q_tile > 0 ? p.q_tile : int64_t(kChunkRows) / G;
   for (int64_t b = 0; b < B; ++b) {
     if (C[b] == 1) continue;
     const int64_t P = L[b] - C[b];
@@ -159,37 +159,58 @@ libra_status build_plan(const libra_plan_desc& d, const int32_t* seq_lens, const
     }
   }
   // Step 9 (chunk units): XCD-affine order.  Tiles of one (b, g) read the same keys, so
-  // they are kept on one XCD (workgroup w runs on XCD w % kNumXcds) to share its L2.
-  // Groups by descending total cost (ties ascending (b, g)) are dealt to the XCD queue
-  // with the least accumulated cost (ties to the lowest queue); inside a group, tiles by
-  // descending cost, ties ascending q_begin; queues are listed one after another.
+  // they are kept on one XCD (workgroup w runs on XCD w % kNumXcds) to share its L2,
+  // unless the group costs more than an eighth of the launch: it is then cut into
+  // contiguous, cost-balanced parts so that every XCD gets work.  Parts by descending
+  // cost (ties ascending (b, g, part)) are dealt to the XCD queue with the least
+  // accumulated cost (ties to the lowest queue); inside a part, tiles by descending
+  // cost, ties ascending q_begin; queues are listed one after another.
   auto cost = [](const Unit& u) { return int64_t(u[U_KV1] - u[U_KV0]) * (u[U_Q1] - u[U_Q0]); };
-  std::vector<std::pair<size_t, size_t>> groups;  // [first, last) in chunks (built in (b, g) order)
-  for (size_t i = 0; i < chunks.size();) {
+  int64_t total_cost = 0;
+  for (const Unit& u : chunks) total_cost += cost(u);
+  const int64_t fair = std::max<int64_t>(1, ceil_div(total_cost, kNumXcds));
+  struct Part { int64_t cost; int32_t b, g, idx; size_t first, last; };  // [first, last) in part_tiles
+  std::vector<Part> parts;
+  std::vector<Unit> part_tiles;  // chunks regrouped part by part
+  part_tiles.reserve(chunks.size());
+  for (size_t i = 0; i < chunks.size();) {  // chunks are built in ascending (b, g, q_begin)
     size_t j = i + 1;
     while (j < chunks.size() && chunks[j][U_B] == chunks[i][U_B] && chunks[j][U_G] == chunks[i][U_G]) ++j;
-    groups.emplace_back(i, j);
+    int64_t c = 0;
+    for (size_t k = i; k < j; ++k) c += cost(chunks[k]);
+    const int64_t n = std::min<int64_t>(int64_t(j - i), ceil_div(c, fair));
+    int64_t before = 0, cur = -1;
+    for (size_t k = i; k < j; ++k) {
+      const int64_t idx = int64_t(__int128(before) * n / c);
+      if (idx != cur) {
+        parts.push_back(Part{0, chunks[k][U_B], chunks[k][U_G], int32_t(idx), part_tiles.size(),
+                             part_tiles.size()});
+        cur = idx;
+      }
+      parts.back().cost += cost(chunks[k]);
+      parts.back().last += 1;
+      part_tiles.push_back(chunks[k]);
+      before += cost(chunks[k]);
+    }
     i = j;
   }
-  std::vector<int64_t> gcost(groups.size(), 0);
-  for (size_t k = 0; k < groups.size(); ++k)
-    for (size_t i = groups[k].first; i < groups[k].second; ++i) gcost[k] += cost(chunks[i]);
-  std::vector<size_t> gorder(groups.size());
-  for (size_t k = 0; k < gorder.size(); ++k) gorder[k] = k;
-  std::sort(gorder.begin(), gorder.end(), [&](size_t a, size_t b) {
-    if (gcost[a] != gcost[b]) return gcost[a] > gcost[b];
-    const Unit &x = chunks[groups[a].first], &y = chunks[groups[b].first];
-    if (x[U_B] != y[U_B]) return x[U_B] < y[U_B];
-    return x[U_G] < y[U_G];
+  std::vector<size_t> porder(parts.size());
+  for (size_t k = 0; k < porder.size(); ++k) porder[k] = k;
+  std::sort(porder.begin(), porder.end(), [&](size_t a, size_t b) {
+    const Part &x = parts[a], &y = parts[b];
+    if (x.cost != y.cost) return x.cost > y.cost;
+    if (x.b != y.b) return x.b < y.b;
+    if (x.g != y.g) return x.g < y.g;
+    return x.idx < y.idx;
   });
   std::vector<std::vector<Unit>> queues(kNumXcds);
   int64_t qcost[kNumXcds] = {0};
-  for (size_t k : gorder) {
+  for (size_t k : porder) {
     int x = 0;
     for (int y = 1; y < kNumXcds; ++y)
       if (qcost[y] < qcost[x]) x = y;
-    qcost[x] += gcost[k];
-    std::vector<Unit> tiles(chunks.begin() + groups[k].first, chunks.begin() + groups[k].second);
+    qcost[x] += parts[k].cost;
+    std::vector<Unit> tiles(part_tiles.begin() + parts[k].first, part_tiles.begin() + parts[k].last);
     std::sort(tiles.begin(), tiles.end(), [&](const Unit& a, const Unit& b) {
       const int64_t ca = cost(a), cb = cost(b);
       if (ca != cb) return ca > cb;

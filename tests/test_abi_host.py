@@ -125,9 +125,8 @@ def test_plan_bit_exact_random(seed):
     _compare(lens, None, G * hkv, hkv, params)
     qlens = [int(rng.choice([1, 1, 2, 17, 300, 1024])) for _ in lens]
     lens2 = [max(L, c) for L, c in zip(lens, qlens)]
-    tpb = max(1, 16 // G)
     params2 = oracle.PlanParams(params.num_cus, params.units_per_cu, params.min_split_pages,
-                                params.max_splits, q_tile=int(rng.integers(0, 16 * tpb + 1)))
+                                params.max_splits, q_tile=int(rng.integers(0, 256 // G + 1)))
     _compare(lens2, qlens, G * hkv, hkv, params2)
 
 
@@ -150,7 +149,7 @@ def test_plan_validation_codes():
     assert _status_of(P, A, 1, 8, 2, [5], [0], 8) == 1              # C = 0
     assert _status_of(P, D, 1, 8, 2, [-1], None, 8) == 1            # negative length
     assert _status_of(P, D, 1, 8, 2, [5], None, 8, 0) == 1          # units_per_cu = 0
-    assert _status_of(P, A, 1, 8, 2, [90], [80], 8, 2, 32, 64, 65) == 2  # q_tile > 16 * 4
+    assert _status_of(P, A, 1, 8, 2, [90], [80], 8, 2, 32, 64, 65) == 2  # q_tile > 256 / 4
     h = P(D, 0, 8, 2, [], None, 8)                                    # empty batch is valid
     assert libra.libra_plan_get_info(h)["n_units"] == 0
     libra.libra_plan_destroy(h)

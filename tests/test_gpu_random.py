@@ -27,12 +27,12 @@ def _case(seed):
     q_lens = None
     if append:
         q_lens = [int(min(L, rng.choice([1, 1, 2, 16, 17, 50, 130]))) for L in lens]
-    tpb = max(1, 16 // g)
+
     params = dict(num_cus=int(rng.choice([4, 16, 64, 256])),
                   units_per_cu=int(rng.integers(1, 5)),
                   min_split_pages=int(rng.choice([1, 2, 4, 16])),
                   max_splits=int(rng.choice([1, 2, 8, 64])),
-                  q_tile=int(rng.choice([0, 1, 16, 16 * tpb])))
+                  q_tile=int(rng.choice([0, 1, 16, 256 // g])))
     return g * hkv, hkv, lens, q_lens, params
 
 

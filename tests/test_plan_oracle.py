@@ -23,25 +23,58 @@ def test_hand_derived_decode_example():
 
 
 def test_hand_derived_append_example():
-    # L = [10, 100], C = [1, 70], Hkv = 2, G = 8 -> T = 16 * (16 // 8) = 32.
+    # L = [10, 100], C = [1, 70], Hkv = 2, G = 8 -> T = floor(256 / 8) = 32.
     # Single row 0: one page, W = 2, target = 4, chunk = 1, n = 1.
     # Chunk row 1: P = 30, tiles [0,32) [32,64) [64,70) with keys [0,62) [0,94) [0,100);
-    # costs 62*32 = 1984, 94*32 = 3008, 100*6 = 600; both KV-head groups cost 5592, so
-    # (1, 0) goes to queue 0 and (1, 1) to queue 1, each listing its tiles 3008, 1984, 600.
+    # costs 62*32 = 1984, 94*32 = 3008, 100*6 = 600; each KV-head group costs 5592 of a
+    # total 11184, so F = ceil(11184 / 8) = 1398 and each group is cut into
+    # n = min(3, ceil(5592 / 1398)) = 3 parts: tile i goes to part floor(S_i * 3 / 5592)
+    # with S = 0, 1984, 4992 -> parts 0, 1, 2, one tile each.  Parts by descending cost,
+    # ties (b, g, part): (1,0,1) (1,1,1) 3008, (1,0,0) (1,1,0) 1984, (1,0,2) (1,1,2) 600,
+    # dealt to the empty queues 0..5 in that order.
     units, info = plan_ref([10, 100], [1, 70], 2, 8,
                            PlanParams(num_cus=4, units_per_cu=1, min_split_pages=1, max_splits=4))
     assert units == [
         (0, 0, 0, 10, 0, 1, 0, 1, -1, 0, 0, 9),
         (0, 1, 0, 10, 0, 1, 0, 1, -1, 0, 0, 9),
         (1, 0, 0, 94, 32, 64, 0, 1, -1, 1, 1, 30),
-        (1, 0, 0, 62, 0, 32, 0, 1, -1, 1, 1, 30),
-        (1, 0, 0, 100, 64, 70, 0, 1, -1, 1, 1, 30),
         (1, 1, 0, 94, 32, 64, 0, 1, -1, 1, 1, 30),
+        (1, 0, 0, 62, 0, 32, 0, 1, -1, 1, 1, 30),
         (1, 1, 0, 62, 0, 32, 0, 1, -1, 1, 1, 30),
+        (1, 0, 0, 100, 64, 70, 0, 1, -1, 1, 1, 30),
         (1, 1, 0, 100, 64, 70, 0, 1, -1, 1, 1, 30),
     ]
-    assert info["xcd_queue_lens"] == [3, 3, 0, 0, 0, 0, 0, 0]
+    assert info["xcd_queue_lens"] == [1, 1, 1, 1, 1, 1, 0, 0]
     assert info["n_single"] == 2 and info["n_chunk"] == 6 and info["q_tile"] == 32
+
+
+def test_hand_derived_group_parts():
+    # One 64-token chunk with no prior, Hkv = 1, G = 16 -> T = 16: four tiles with keys
+    # 16, 32, 48, 64 and costs 256, 512, 768, 1024 (total 2560, F = 320).  The group is cut
+    # into n = min(4, ceil(2560 / 320)) = 4 parts at floor(S_i * 4 / 2560), S = 0, 256,
+    # 768, 1536 -> parts 0, 0, 1, 2: {256, 512} = 768, {768}, {1024}.  Dealt by
+    # descending cost: part 2 (1024) -> queue 0, part 0 (768; ties by part index) ->
+    # queue 1, part 1 (768) -> queue 2; part 0 lists its tiles by descending cost.
+    units, info = plan_ref([64], [64], 1, 16, PlanParams())
+    assert [(u[2], u[3], u[4], u[5]) for u in units] == [
+        (0, 64, 48, 64), (0, 32, 16, 32), (0, 16, 0, 16), (0, 48, 32, 48)]
+    assert info["xcd_queue_lens"] == [1, 2, 1, 0, 0, 0, 0, 0]
+
+
+def test_few_groups_fill_every_queue():
+    # A recompute prefill with 4 KV heads has 4 (b, g) groups; each is larger than an
+    # eighth of the work and is cut into parts, so all 8 XCD queues get tiles and their
+    # costs differ by at most the largest single part.
+    units, info = plan_ref([40960], [40960], 4, 7, PlanParams())
+    lens = info["xcd_queue_lens"]
+    assert all(n > 0 for n in lens)
+    chunks = units[info["n_single"]:]
+    cost = [(u[3] - u[2]) * (u[5] - u[4]) for u in chunks]
+    qcost, pos = [], 0
+    for n in lens:
+        qcost.append(sum(cost[pos:pos + n]))
+        pos += n
+    assert max(qcost) - min(qcost) <= 0.02 * sum(cost)
 
 
 def check_invariants(seq_lens, q_lens, hkv, group, params):
@@ -59,27 +92,30 @@ def check_invariants(seq_lens, q_lens, hkv, group, params):
     cost = lambda u: (u[3] - u[2]) * (u[5] - u[4])
     lens = info["xcd_queue_lens"]
     assert sum(lens) == len(chunks)
-    seen = set()
+    seen = {}
     pos = 0
     qcost = []
     for n in lens:
         q = chunks[pos:pos + n]
         pos += n
         qcost.append(sum(cost(u) for u in q))
-        i = 0
-        while i < len(q):
-            j = i
-            while j < len(q) and q[j][:2] == q[i][:2]:
-                j += 1
-            key = q[i][:2]
-            assert key not in seen
-            seen.add(key)
-            c = [cost(u) for u in q[i:j]]
-            assert c == sorted(c, reverse=True)
-            i = j
+        for u in q:
+            seen.setdefault(u[:2], []).append((len(qcost) - 1, pos - n + q.index(u)))
     if chunks:
-        biggest_group = max(sum(cost(u) for u in chunks if u[:2] == k) for k in seen)
-        assert max(qcost) - min(qcost) <= biggest_group
+        total = sum(cost(u) for u in chunks)
+        fair = -(-total // 8)
+        for key, where in seen.items():
+            gcost = sum(cost(u) for u in chunks if u[:2] == key)
+            if gcost <= fair:
+                # an uncut group: one queue, contiguous, tiles by descending cost
+                assert len({x for x, _ in where}) == 1
+                idx = sorted(i for _, i in where)
+                assert idx == list(range(idx[0], idx[0] + len(idx)))
+                c = [cost(chunks[i]) for i in idx]
+                assert c == sorted(c, reverse=True)
+        # dealing bound: queues differ by at most one part, and a part costs at most
+        # F plus one tile
+        assert max(qcost) - min(qcost) <= fair + max(cost(u) for u in chunks)
     # single rows: splits tile [0, L) exactly, page aligned, non-empty unless L = 0
     slots = set()
     for b in range(B):
