@@ -63,16 +63,22 @@ def flops(batch) -> int:
 
 def kernel_source_sha() -> str:
     h = hashlib.sha256()
-    for f in ("decode.hip", "internal.h", "plan.cpp"):   # the plan sets the partial traffic
+    for f in ("decode.hip", "internal.h"):
         with open(os.path.join(ROOT, "paper_2606_03077_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
 
 
-def traffic_from_profile(workload: str):
+def plan_sha(units: np.ndarray) -> str:
+    """Hash of a plan's unit table: the decode kernel's traffic depends on it (partials)."""
+    return hashlib.sha256(np.ascontiguousarray(units, dtype=np.int32).tobytes()).hexdigest()[:16]
+
+
+def traffic_from_profile(workload: str, units_sha: str):
     """HBM bytes per launch of the decode kernel from committed rocprofv3 counters.
 
-    Null unless profiles/counters.json was taken on the current kernel and plan source.
+    Null unless profiles/counters.json was taken on the current kernel source and on a
+    plan with the same unit table.
     """
     try:
         with open(PROFILE_COUNTERS) as f:
@@ -80,7 +86,7 @@ def traffic_from_profile(workload: str):
     except (OSError, ValueError):
         return None
     e = c.get("decode_kernel", {}).get(workload)
-    if not e or e.get("source_sha") != kernel_source_sha():
+    if not e or e.get("source_sha") != kernel_source_sha() or e.get("plan_sha") != units_sha:
         return None
     return e.get("hbm_bytes_per_launch")
 
@@ -700,7 +706,8 @@ def main():
         achieved = ab["total"] / (kernel_avg_ms[kern] * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                "traffic": traffic_from_profile(args.workload), "kernel": "decode_kernel",
+                "traffic": traffic_from_profile(args.workload, plan_sha(libra.libra_plan_get_units(plan))),
+                "kernel": "decode_kernel",
                 "algorithmic_bytes_per_launch": ab["total"]}
     roof["kernel_avg_ms"] = round(kernel_avg_ms[kern], 5)
     roof["other_kernels_avg_ms"] = {k: round(v, 5) for k, v in kernel_avg_ms.items() if k != kern}
