@@ -252,19 +252,43 @@ def test_recompute_prefill_empty_prior(chunk):
     cache.close()
 
 
-def test_recompute_prefill_full_length_sampled():
-    """The 40,960-token recompute at full size; the oracle checks sampled query rows."""
-    H.say("[case] prefill 40960 full size")
-    b = wl.make_batch("prefill")
+@pytest.mark.parametrize("hq,hkv", [(28, 4), (16, 1), (48, 8), (96, 8), (24, 8)])
+def test_recompute_prefill_head_shapes(hq, hkv):
+    """Fewer than eight (sequence, KV head) groups, whose tiles the plan cuts into parts
+    over all XCD queues, and groups G that do not divide 16 (query tiles of
+    floor(256 / G) tokens whose column blocks span token boundaries)."""
+    chunk = 1500
+    from oracle.plan import plan_ref, PlanParams
+    _, info = plan_ref([chunk], [chunk], hkv, hq // hkv, PlanParams())
+    assert info["q_tile"] == 256 // (hq // hkv)
+    if hkv < 8:
+        assert all(n > 0 for n in info["xcd_queue_lens"])   # the groups were cut into parts
+    H.say(f"[case] prefill P=0 C={chunk} hq={hq} hkv={hkv}")
+    b = wl.custom_batch([chunk], q_lens=[chunk], num_q_heads=hq, num_kv_heads=hkv,
+                        seed=hq * 100 + hkv, append=True)
+    o, lse, cache, _ = H.run(b)
+    ro, rl, k_after, v_after = _append_oracle(b)
+    H.assert_parity(o, lse, ro, rl, label=f"prefill {hq}/{hkv}")
+    k2, v2 = cache.unpack()
+    assert np.array_equal(k2, k_after) and np.array_equal(v2, v_after)
+    cache.close()
+
+
+@pytest.mark.parametrize("hq,hkv,rows", [(40, 8, [0, 1, 47, 48, 50, 51, 4095, 20000, 40959]),
+                                         (28, 4, [0, 1, 35, 36, 37, 4095, 20000, 40959])])
+def test_recompute_prefill_full_length_sampled(hq, hkv, rows):
+    """The 40,960-token recompute at full size; the oracle checks sampled query rows
+    (around tile boundaries, and for 4 KV heads, with the groups cut into parts)."""
+    H.say(f"[case] prefill 40960 full size hq={hq} hkv={hkv}")
+    b = wl.make_batch("prefill", num_q_heads=hq, num_kv_heads=hkv)
     o, lse, cache, _ = H.run(b)
     cache.close()
     k_all = b.k_new  # prior is empty: the new tokens are the whole context
     v_all = b.v_new
-    rows = [0, 1, 47, 48, 4095, 20000, 40959]
     from oracle.attention import attend, bf16_bits_to_f64
-    G = 5
+    G = hq // hkv
     for r in rows:
-        for h in (0, 7, 21, 39):
+        for h in (0, G - 1, G, hq - 1):
             g = h // G
             ro, rl = attend(bf16_bits_to_f64(b.q[r, h])[None], bf16_bits_to_f64(k_all[:r + 1, g]),
                             bf16_bits_to_f64(v_all[:r + 1, g]), b.scale)
