@@ -61,21 +61,25 @@ def flops(batch) -> int:
     return 4 * 128 * pairs
 
 
-def kernel_source_sha() -> str:
+KERNEL_SOURCES = {"decode_kernel": ("decode.hip", "internal.h"),
+                  "chunk_kernel": ("chunk.hip", "internal.h")}
+
+
+def kernel_source_sha(kernel: str = "decode_kernel") -> str:
     h = hashlib.sha256()
-    for f in ("decode.hip", "internal.h"):
+    for f in KERNEL_SOURCES[kernel]:
         with open(os.path.join(ROOT, "paper_2606_03077_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
 
 
 def plan_sha(units: np.ndarray) -> str:
-    """Hash of a plan's unit table: the decode kernel's traffic depends on it (partials)."""
+    """Hash of a plan's unit table: a kernel's traffic depends on it (partials, tiles)."""
     return hashlib.sha256(np.ascontiguousarray(units, dtype=np.int32).tobytes()).hexdigest()[:16]
 
 
-def traffic_from_profile(workload: str, units_sha: str):
-    """HBM bytes per launch of the decode kernel from committed rocprofv3 counters.
+def traffic_from_profile(kernel: str, workload: str, units_sha: str):
+    """HBM bytes per launch of `kernel` from committed rocprofv3 counters.
 
     Null unless profiles/counters.json was taken on the current kernel source and on a
     plan with the same unit table.
@@ -85,8 +89,8 @@ def traffic_from_profile(workload: str, units_sha: str):
             c = json.load(f)
     except (OSError, ValueError):
         return None
-    e = c.get("decode_kernel", {}).get(workload)
-    if not e or e.get("source_sha") != kernel_source_sha() or e.get("plan_sha") != units_sha:
+    e = c.get(kernel, {}).get(workload)
+    if not e or e.get("source_sha") != kernel_source_sha(kernel) or e.get("plan_sha") != units_sha:
         return None
     return e.get("hbm_bytes_per_launch")
 
@@ -699,14 +703,17 @@ def main():
         achieved = work / (kernel_avg_ms[kern] * 1e-3) / 1e12
         roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4),
-                "traffic": None, "kernel": "chunk_kernel",
+                "traffic": traffic_from_profile("chunk_kernel", args.workload,
+                                                plan_sha(libra.libra_plan_get_units(plan))),
+                "kernel": "chunk_kernel",
                 "algorithmic_flops_per_launch": work}
     else:
         kern = "decode"
         achieved = ab["total"] / (kernel_avg_ms[kern] * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                "traffic": traffic_from_profile(args.workload, plan_sha(libra.libra_plan_get_units(plan))),
+                "traffic": traffic_from_profile("decode_kernel", args.workload,
+                                                plan_sha(libra.libra_plan_get_units(plan))),
                 "kernel": "decode_kernel",
                 "algorithmic_bytes_per_launch": ab["total"]}
     roof["kernel_avg_ms"] = round(kernel_avg_ms[kern], 5)
