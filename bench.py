@@ -61,8 +61,9 @@ def flops(batch) -> int:
     return 4 * 128 * pairs
 
 
-KERNEL_SOURCES = {"decode_kernel": ("decode.hip", "internal.h"),
-                  "chunk_kernel": ("chunk.hip", "internal.h")}
+# The device code of each kernel: its source and the table formats it reads.
+KERNEL_SOURCES = {"decode_kernel": ("decode.hip", "tables.h"),
+                  "chunk_kernel": ("chunk.hip", "tables.h")}
 
 
 def kernel_source_sha(kernel: str = "decode_kernel") -> str:

@@ -261,10 +261,13 @@ libra_status libra_plan_get_info(libra_plan plan, libra_plan_info* info);
  * and the float32 partial results of split rows). */
 size_t libra_plan_workspace_bytes(libra_plan plan);
 /* Copies the plan's tables into `workspace` (device) on `stream`.  Decode / append calls
- * do this themselves when the workspace they get is not the one last uploaded to;
+ * do this themselves unless this plan was the last one to upload to that address;
  * calling it explicitly once per batch step lets every layer's call skip it.  The
- * workspace then belongs to this plan until another upload; calls that share a
- * workspace must be ordered on one stream. */
+ * workspace then belongs to this plan until another plan uploads to it (plans may take
+ * turns on one workspace; each call of another plan re-uploads).  Calls that share a
+ * workspace must be ordered on one stream.  Memory that is freed and allocated again at
+ * the same address, or written by anything but this library, no longer holds the tables:
+ * call libra_plan_upload on it before the next decode / append call. */
 libra_status libra_plan_upload(libra_plan plan, void* workspace, size_t ws_bytes, void* stream);
 /* Waits for the plan's pending upload (if any), then frees it. */
 void libra_plan_destroy(libra_plan plan);

@@ -1,10 +1,13 @@
 // extern "C" entry points of libra (declared and documented in include/libra.h).
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstring>
+#include <iterator>
 #include <mutex>
 #include <new>
 #include <string>
+#include <unordered_map>
 #include <vector>
 
 #include "internal.h"
@@ -102,23 +105,26 @@ libra_status check_layout(const libra_kv_layout_desc* d) {
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 
-// Largest page index + 1 the plan's units and writes touch, per the block table.
-int64_t plan_pages_needed(const Plan& P) {
-  int64_t need = 0;
-  const int n = P.info.n_units;
-  for (int i = 0; i < n; ++i) {
-    const int32_t* u = &P.units[size_t(i) * kUnitInts];
-    need = std::max<int64_t>(need, (int64_t(u[U_KV1]) + kPage - 1) / kPage);
-  }
-  for (int i = 0; i < P.info.n_write_tiles; ++i)
-    need = std::max<int64_t>(need, int64_t(P.writes[size_t(i) * kWriteInts + W_PAGE]) + 1);
-  return need;
+// Which plan's tables each workspace holds, by plan id: a call skips the table upload
+// only if its own plan was the last to upload to that workspace, so plans that take
+// turns on one workspace never read each other's tables.
+struct WorkspaceOwners {
+  std::mutex mu;
+  std::unordered_map<uintptr_t, uint64_t> owner;
+};
+WorkspaceOwners g_ws;
+std::atomic<uint64_t> g_next_plan_id{1};
+
+bool holds_tables(const void* ws, uint64_t id) {
+  std::lock_guard<std::mutex> lk(g_ws.mu);
+  auto it = g_ws.owner.find(reinterpret_cast<uintptr_t>(ws));
+  return it != g_ws.owner.end() && it->second == id;
 }
 
 // Copies the plan's tables into ws unless ws already holds them (or always, if forced).
 libra_status upload(Plan& P, void* ws, size_t ws_bytes, hipStream_t s, bool force = true) {
   std::lock_guard<std::mutex> lk(P.upload_mu);
-  if (!force && P.uploaded_ws == ws) return LIBRA_OK;
+  if (!force && holds_tables(ws, P.id)) return LIBRA_OK;
   if (!ws) return set_error(LIBRA_E_INVAL, "workspace is NULL");
   if (reinterpret_cast<uintptr_t>(ws) % kWorkspaceAlign)
     return set_error(LIBRA_E_INVAL, "workspace must be 256-byte aligned");
@@ -154,7 +160,10 @@ libra_status upload(Plan& P, void* ws, size_t ws_bytes, hipStream_t s, bool forc
   }
   e = hipEventRecord(P.upload_done, s);
   if (e != hipSuccess) return hip_error(e, "hipEventRecord");
-  P.uploaded_ws = ws;
+  {
+    std::lock_guard<std::mutex> lk2(g_ws.mu);
+    g_ws.owner[reinterpret_cast<uintptr_t>(ws)] = P.id;
+  }
   return LIBRA_OK;
 }
 
@@ -174,7 +183,7 @@ libra_status check_call(const KvLayout* L, const Plan* P, int mode, const void* 
     if (!q || !out) return set_error(LIBRA_E_INVAL, "q / out is NULL");
     if (!aligned16(q) || !aligned16(out)) return set_error(LIBRA_E_INVAL, "q / out must be 16-byte aligned");
   }
-  const int64_t need = plan_pages_needed(*P);
+  const int64_t need = P->pages_needed;
   if (need > 0) {
     if (!bt) return set_error(LIBRA_E_INVAL, "block_table is NULL");
     if (bt_stride < need)
@@ -390,6 +399,7 @@ libra_status libra_splitkv_plan(const libra_plan_desc* desc, const int32_t* seq_
 
   auto* P = new (std::nothrow) libra_plan_s();
   if (!P) return set_error(LIBRA_E_NOMEM, "plan allocation failed");
+  P->id = g_next_plan_id.fetch_add(1);
   libra_status st;
   try {
     st = build_plan(d, seq_lens_host, q_lens_host, p, P);
@@ -429,6 +439,11 @@ void libra_plan_destroy(libra_plan plan) {
   if (plan->upload_done) {
     (void)hipEventSynchronize(plan->upload_done);
     (void)hipEventDestroy(plan->upload_done);
+  }
+  {
+    std::lock_guard<std::mutex> lk(g_ws.mu);
+    for (auto it = g_ws.owner.begin(); it != g_ws.owner.end();)
+      it = it->second == plan->id ? g_ws.owner.erase(it) : std::next(it);
   }
   if (plan->pinned) (void)hipHostFree(plan->pinned);
   delete plan;

@@ -9,31 +9,9 @@
 #include <vector>
 
 #include "libra.h"
+#include "tables.h"
 
 namespace libra {
-
-constexpr int kPage = LIBRA_PAGE_SIZE;     // tokens per page
-constexpr int kDim = LIBRA_HEAD_DIM;       // channels per head
-constexpr int kTileElems = kPage * kDim;   // bf16 elements per (page, head) tile
-constexpr int kTileBytes = kTileElems * 2; // 4 KiB
-constexpr int kUnitInts = LIBRA_UNIT_INTS;
-
-// Unit record fields (int32), in table order.
-enum UnitField : int {
-  U_B = 0, U_G, U_KV0, U_KV1, U_Q0, U_Q1, U_SPLIT, U_NSPLIT, U_PART, U_ROW0, U_KIND, U_PRIOR
-};
-constexpr int kKindSingle = 0;
-constexpr int kKindChunk = 1;
-constexpr int kNumXcds = 8;  // MI355X: workgroup w is dispatched to XCD w % 8
-constexpr int kChunkRows = 256;  // (token, head) rows of one chunk-kernel tile
-
-// Append cache-write table: one record per (sequence, page) the new tokens touch.
-enum WriteField : int { W_B = 0, W_PAGE, W_SLOT0, W_SLOT1, W_ROW, W_PAD0, W_PAD1, W_PAD2 };
-constexpr int kWriteInts = 8;
-
-// Split-merge table: one record per (sequence, KV head) whose KV range was split.
-enum MergeField : int { M_B = 0, M_G, M_N, M_PART, M_ROW, M_PAD0, M_PAD1, M_PAD2 };
-constexpr int kMergeInts = 8;
 
 struct Plan {
   int32_t mode = LIBRA_MODE_DECODE;
@@ -52,12 +30,13 @@ struct Plan {
          off_part_lse = 0;
   size_t ws_bytes = 0;
   size_t upload_bytes = 0;  // bytes of [units | writes | merges | xcd map] from the host
+  int64_t pages_needed = 0; // block-table columns the units and writes read (per row, max)
+  uint64_t id = 0;          // process-unique, set at creation: which plan a workspace holds
 
   // Upload state (guarded by upload_mu: calls on one plan may come from several threads).
   std::mutex upload_mu;
   void* pinned = nullptr;         // host staging copy of [units | writes | merges | xcd map]
   hipEvent_t upload_done = nullptr;
-  void* uploaded_ws = nullptr;
 };
 
 struct KvLayout {

@@ -270,6 +270,13 @@ libra_status build_plan(const libra_plan_desc& d, const int32_t* seq_lens, const
     }
   }
 
+  // Block-table columns the kernels read: every unit's pages and every written page.
+  P.pages_needed = 0;
+  for (size_t i = 0; i < P.units.size(); i += kUnitInts)
+    P.pages_needed = std::max<int64_t>(P.pages_needed, ceil_div(P.units[i + U_KV1], kPage));
+  for (size_t i = 0; i < P.writes.size(); i += kWriteInts)
+    P.pages_needed = std::max<int64_t>(P.pages_needed, int64_t(P.writes[i + W_PAGE]) + 1);
+
   libra_plan_info& I = P.info;
   std::memset(&I, 0, sizeof(I));
   I.n_single = int32_t(singles.size());

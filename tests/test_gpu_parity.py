@@ -226,6 +226,40 @@ def test_split_merge_sees_fresh_partials_when_workspace_is_reused():
     libra.libra_plan_destroy(plan)
 
 
+def test_two_plans_take_turns_on_one_workspace():
+    """Two plans with different unit tables share one workspace without explicit uploads:
+    each call must re-upload its own tables when the other plan wrote the workspace last.
+    (Both batches have 5 rows and equally wide block tables padded with valid spare pages,
+    so even a stale table would stay in bounds and show up as a parity failure.)"""
+    lens_a = [3000, 17, 5000, 129, 2048]
+    lens_b = [100, 2900, 40, 4999, 1000]
+    H.say("[case] two plans, one workspace")
+    ba = wl.custom_batch(lens_a, num_q_heads=28, num_kv_heads=4, seed=31)
+    bb = wl.custom_batch(lens_b, num_q_heads=28, num_kv_heads=4, seed=32)
+    assert ba.block_table.shape == bb.block_table.shape
+    kw = dict(num_cus=64, units_per_cu=1, min_split_pages=2)
+    pa = libra.libra_splitkv_plan(libra.LIBRA_MODE_DECODE, 5, 28, 4, lens_a, None, **kw)
+    pb = libra.libra_splitkv_plan(libra.LIBRA_MODE_DECODE, 5, 28, 4, lens_b, None, **kw)
+    assert not np.array_equal(libra.libra_plan_get_units(pa), libra.libra_plan_get_units(pb))
+    n = max(libra.libra_plan_workspace_bytes(pa), libra.libra_plan_workspace_bytes(pb))
+    ws = torch.empty(n, dtype=torch.uint8, device="cuda")
+    assert ws.data_ptr() % 256 == 0
+    cases = {"a": (ba, pa, H.DeviceCache(ba), _decode_oracle(ba)),
+             "b": (bb, pb, H.DeviceCache(bb), _decode_oracle(bb))}
+    out = torch.empty((5, 28, 128), dtype=torch.int16, device="cuda")
+    lse = torch.empty((5, 28), dtype=torch.float32, device="cuda")
+    for key in "abaabba":
+        b, plan, cache, ref = cases[key]
+        libra.libra_decode_attn(cache.layout, plan, H.u16_to_dev(b.q), cache.bt, cache.bt_stride,
+                                5, 28, b.scale, ws, out, lse)
+        torch.cuda.synchronize()
+        H.assert_parity(H.bf16_dev_to_f64(out), lse.cpu().numpy().astype(np.float64), ref[0],
+                        ref[1], label=f"plan {key}")
+    for b, plan, cache, _ in cases.values():
+        cache.close()
+        libra.libra_plan_destroy(plan)
+
+
 def test_append_prior_longer_than_staged_block_table():
     """A chunk whose keys span more pages than the chunk kernel stages in LDS (4096)."""
     prior, chunk = 66000, 100
