@@ -155,6 +155,14 @@ def check_invariants(seq_lens, q_lens, hkv, group, params):
                 assert u[F["row0"]] == row0[b] and u[5] - u[4] <= info["q_tile"]
     total = sum(u[3] - u[2] for u in singles)
     assert total == hkv * sum(seq_lens[b] for b in range(B) if C[b] == 1)
+    if info["balanced"]:
+        # one wave: at most S units, and the largest piece within 1.5x the mean share
+        S = params.num_cus * params.units_per_cu
+        R = S // hkv
+        assert len(singles) <= R * hkv <= S
+        pages = [-(-(u[3] - u[2]) // 16) for u in singles]
+        wp = sum(-(-seq_lens[b] // 16) for b in range(B) if C[b] == 1)
+        assert 2 * max(pages) * R <= 3 * wp
     return units, info
 
 
