@@ -173,28 +173,45 @@ __global__ __launch_bounds__(kThreads) void page_copy_kernel(uint4* __restrict__
 
 }  // namespace
 
+// One workgroup per tile; a 1-D grid holds at most 2^32 - 1 work-items, so long page
+// ranges go in launches of kMaxTilesPerLaunch tiles (the long-tailed batch packs in 3).
+constexpr int64_t kMaxTilesPerLaunch = int64_t(1) << 18;
+
 hipError_t launch_pack(const KvLayout& L, const void* k_src, const void* v_src, int64_t first,
                        int64_t n, hipStream_t s) {
   const int hkv = L.desc.num_kv_heads;
   const int64_t tiles = n * hkv;
-  if (tiles == 0) return hipSuccess;
-  hipLaunchKernelGGL(pack_kernel, dim3(unsigned(tiles)), dim3(kThreads), 0, s,
-                     static_cast<const uint16_t*>(k_src), static_cast<const uint16_t*>(v_src),
-                     static_cast<uint16_t*>(L.desc.k_cache), static_cast<uint16_t*>(L.desc.v_cache),
-                     first * hkv);
-  return hipGetLastError();
+  const uint16_t* ks = static_cast<const uint16_t*>(k_src);
+  const uint16_t* vs = static_cast<const uint16_t*>(v_src);
+  for (int64_t t0 = 0; t0 < tiles; t0 += kMaxTilesPerLaunch) {
+    const int64_t nt = std::min(kMaxTilesPerLaunch, tiles - t0);
+    const size_t off = size_t(t0) * kTileElems;
+    hipLaunchKernelGGL(pack_kernel, dim3(unsigned(nt)), dim3(kThreads), 0, s, ks ? ks + off : ks,
+                       vs ? vs + off : vs, static_cast<uint16_t*>(L.desc.k_cache),
+                       static_cast<uint16_t*>(L.desc.v_cache), first * hkv + t0);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 hipError_t launch_unpack(const KvLayout& L, void* k_dst, void* v_dst, int64_t first, int64_t n,
                          hipStream_t s) {
   const int hkv = L.desc.num_kv_heads;
   const int64_t tiles = n * hkv;
-  if (tiles == 0) return hipSuccess;
-  hipLaunchKernelGGL(unpack_kernel, dim3(unsigned(tiles)), dim3(kThreads), 0, s,
-                     static_cast<const uint16_t*>(L.desc.k_cache),
-                     static_cast<const uint16_t*>(L.desc.v_cache), static_cast<uint16_t*>(k_dst),
-                     static_cast<uint16_t*>(v_dst), first * hkv);
-  return hipGetLastError();
+  uint16_t* kd = static_cast<uint16_t*>(k_dst);
+  uint16_t* vd = static_cast<uint16_t*>(v_dst);
+  for (int64_t t0 = 0; t0 < tiles; t0 += kMaxTilesPerLaunch) {
+    const int64_t nt = std::min(kMaxTilesPerLaunch, tiles - t0);
+    const size_t off = size_t(t0) * kTileElems;
+    hipLaunchKernelGGL(unpack_kernel, dim3(unsigned(nt)), dim3(kThreads), 0, s,
+                       static_cast<const uint16_t*>(L.desc.k_cache),
+                       static_cast<const uint16_t*>(L.desc.v_cache), kd ? kd + off : kd,
+                       vd ? vd + off : vd, first * hkv + t0);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 hipError_t launch_gather(const KvLayout& L, const int32_t* bt, int32_t stride, const int32_t* cu,
