@@ -5,13 +5,14 @@
 // token-major, packed 16 to a matrix column block whatever G is (a block may hold the
 // end of one token's heads and the start of the next's); each wave owns 2 column blocks,
 // so a workgroup covers 256 rows, i.e. up to floor(256 / G) tokens.  Keys are visited
-// 64 at a time: the step's eight 4 KiB tiles (K and V of 4 pages) are loaded into
-// registers two steps ahead, staged in LDS (three stages) and shared by the 8 waves; V
-// is interleaved by page pair on the way in so that each PV operand is a single 16-byte
-// LDS read.  Each wave works through a step by page pairs: the pair's probabilities,
-// the next step's scores of the same two pages (written over the ones just consumed, so
-// one score set suffices) and the pair's PV, which lets exps overlap score and PV
-// MFMAs.  Per page and column block:
+// 64 at a time and staged in LDS (four stages), shared by the 8 waves: the step's four
+// 4 KiB K tiles are copied from memory straight into LDS three steps ahead
+// (global_load_lds_dwordx4, no registers), its four V tiles are loaded into registers
+// two steps ahead and written to LDS interleaved by page pair, so that each PV operand
+// is a single 16-byte LDS read.  Each wave works through a step by page pairs: the
+// pair's probabilities, the next step's scores of the same two pages (written over the
+// ones just consumed, so one score set suffices) and the pair's PV, which lets exps
+// overlap score and PV MFMAs.  Per page and column block:
 //   S^T = K . Q^T (4 mfma 16x16x32), and per page pair O^T += V^T . P^T (8 mfma 16x16x32
 //   over 32 keys).
 // Softmax runs online in base 2.  The running maximum is only moved (and the
@@ -41,7 +42,7 @@ static_assert(kChunkRows == 16 * kNB * kWaves, "the plan's tile rows are the ker
 constexpr int kStepPages = 4;    // pages (16 keys each) per softmax step
 constexpr float kTau = 8.f;      // lazy-rescale threshold, base-2 logits
 constexpr int kMaxIds = 4096;    // block-table entries staged in LDS (64K keys)
-constexpr int kBufs = 3;         // LDS stages: step n (V), step n + 1 (K), step n + 2 (landing)
+constexpr int kBufs = 4;         // LDS stages, indexed by step & 3
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
@@ -77,9 +78,26 @@ void chunk_kernel(ChunkArgs A) {
   // V: [buffer][page pair][t][half][lane] x {page 2h bytes, page 2h+1 bytes}: for channel
   // block db = 2 t + half, lane l's 16 bytes are exactly its PV A operand (4 slots of
   // each page of the pair), so the PV loop reads operands with one ds_read_b128.
-  __shared__ uint4 ldk[kBufs][kStepPages][256];
-  __shared__ uint2 ldv[kBufs][kStepPages / 2][4][2][64][2];
+  // One array per K stage: the direct memory-to-LDS copies of one stage then never
+  // make the compiler wait before LDS reads of another.
+  __shared__ __align__(16) uint4 ldk0[kStepPages][256];
+  __shared__ __align__(16) uint4 ldk1[kStepPages][256];
+  __shared__ __align__(16) uint4 ldk2[kStepPages][256];
+  __shared__ __align__(16) uint4 ldk3[kStepPages][256];
+  __shared__ __align__(16) uint2 ldv[kBufs][kStepPages / 2][4][2][64][2];
   __shared__ __align__(16) int lds_ids[kMaxIds];  // the tile's block-table row
+  using S0 = std::integral_constant<int, 0>;
+  using S1 = std::integral_constant<int, 1>;
+  using S2 = std::integral_constant<int, 2>;
+  using S3 = std::integral_constant<int, 3>;
+  // K stage s & 3 (s a compile-time step index).
+  auto kst = [&](auto s_tag) -> uint4 (&)[kStepPages][256] {
+    constexpr int st = decltype(s_tag)::value & 3;
+    if constexpr (st == 0) return ldk0;
+    else if constexpr (st == 1) return ldk1;
+    else if constexpr (st == 2) return ldk2;
+    else return ldk3;
+  };
 
   const int xcd = blockIdx.x % kNumXcds;
   const int slot = blockIdx.x / kNumXcds;
@@ -126,51 +144,79 @@ void chunk_kernel(ChunkArgs A) {
   const int npages = (kv1 + kPage - 1) / kPage;
   const int nsteps = (npages + kStepPages - 1) / kStepPages;
   const int32_t* btrow = A.bt + int64_t(b) * A.bt_stride;
-  const int half = tid >> 8;          // 0: this thread stages K tiles, 1: V tiles
-  const int elem = tid & 255;         // uint4 index inside a tile
-  // This thread's 16 bytes of tile (page 0, head g); page p adds p * page_bytes (one
-  // 32 x 32 -> 64-bit multiply-add per load; num_kv_heads <= 1024 keeps it in 32 bits).
-  const char* lane_base = reinterpret_cast<const char*>(half ? A.v_cache : A.k_cache) +
-                          size_t(g) * kTileBytes + size_t(elem) * 16;
+  // Page p of head g starts p * page_bytes past the head's first tile (one 32 x 32 ->
+  // 64-bit multiply-add per load; num_kv_heads <= 1024 keeps it in 32 bits).
   const uint32_t page_bytes = uint32_t(A.hkv) * kTileBytes;
   const int first_tok = prior + q0;   // smallest query position of the tile
   // Steps whose first key is past this need the causal / length mask.
   const int mask_key0 = min(first_tok - (kStepPages * kPage - 1), kv1 - kStepPages * kPage);
 
-  // Thread t stages uint4 `elem` of the K (t < 256) or V tile of each page of a step.
-  // The step's 4 page ids come from LDS in one broadcast read; pages past the end
-  // re-read the last page (the id row is padded with it), so the loads stay branch-free
-  // and asynchronous; their keys are >= kv1, so they are masked and their V zeroed.
-  auto fetch = [&](int step, uint4 (&r)[kStepPages]) {
+  // Staging of step `step` (its 4 page ids come from LDS in one broadcast read; pages
+  // past the end re-read the last page, the id row being padded with it, so the loads
+  // stay branch-free; their keys are >= kv1, so they are masked and their V zeroed).
+  // K goes from memory straight into LDS stage step & 3: wave w moves 1 KiB chunks 2w and
+  // 2w + 1 of the step's four 4 KiB K tiles with global_load_lds_dwordx4 (each lane 16 B,
+  // written at the chunk's LDS base + 16 * lane, i.e. the tile as stored).  V comes into
+  // registers: thread t holds uint4 `elem` = t % 256 of both pages of pair t / 256, and
+  // stash() writes them interleaved (one 16-byte LDS store per half).
+  const int vpair = tid >> 8;          // page pair of the step this thread stages V for
+  const int elem = tid & 255;          // uint4 index inside a tile
+  const char* v_lane = reinterpret_cast<const char*>(A.v_cache) + size_t(g) * kTileBytes +
+                       size_t(elem) * 16;
+  const char* k_lane = reinterpret_cast<const char*>(A.k_cache) + size_t(g) * kTileBytes +
+                       size_t(lane) * 16;
+  // The step's 4 page ids (from LDS, one broadcast read; global memory past the staged
+  // row, uniform and rare).
+  auto step_ids = [&](int step, int (&ids)[kStepPages]) {
     const int p0 = step * kStepPages;
-    int ids[kStepPages];
     if (p0 + kStepPages <= kMaxIds) {
       const int4 v = *reinterpret_cast<const int4*>(&lds_ids[p0]);
       ids[0] = v.x;
       ids[1] = v.y;
       ids[2] = v.z;
       ids[3] = v.w;
-    } else {  // rows longer than the staged ids (uniform, rare)
+    } else {
 #pragma unroll
       for (int j = 0; j < kStepPages; ++j)
         ids[j] = __builtin_amdgcn_readfirstlane(btrow[min(p0 + j, npages - 1)]);
     }
-#pragma unroll
-    for (int j = 0; j < kStepPages; ++j)
-      r[j] = *reinterpret_cast<const uint4*>(lane_base + uint64_t(uint32_t(ids[j])) * page_bytes);
   };
-  auto stash = [&](int buf, const uint4 (&r)[kStepPages]) {
-    if (half == 0) {
+  // V of `step` into registers (compiler-tracked loads).
+  auto fetch_v = [&](int step, uint4 (&r)[2]) {
+    int ids[kStepPages];
+    step_ids(step, ids);
 #pragma unroll
-      for (int j = 0; j < kStepPages; ++j) ldk[buf][j][elem] = r[j];
-    } else {
-      const int t = elem >> 6, ln = elem & 63;
+    for (int jj = 0; jj < 2; ++jj)
+      r[jj] = *reinterpret_cast<const uint4*>(
+          v_lane + uint64_t(uint32_t(ids[2 * vpair + jj])) * page_bytes);
+  };
+  // K of `step` straight into LDS stage stage_tag & 3 (global_load_lds_dwordx4: lane l's
+  // 16 bytes land at the chunk's LDS base, held in m0, + 16 l).  Written as inline
+  // assembly so that the compiler does not guard every later LDS access with a wait for
+  // these copies; their completion is ordered by hand: vmcnt counts them in issue order
+  // with the other vector-memory loads, and the wait before each barrier covers them.
+  auto copy_k = [&](int step, auto stage_tag) {
+    int ids[kStepPages];
+    step_ids(step, ids);
 #pragma unroll
-      for (int j = 0; j < kStepPages; ++j) {
-        ldv[buf][j >> 1][t][0][ln][j & 1] = make_uint2(r[j].x, r[j].y);
-        ldv[buf][j >> 1][t][1][ln][j & 1] = make_uint2(r[j].z, r[j].w);
-      }
+    for (int c2 = 0; c2 < 2; ++c2) {
+      const int c = 2 * wave + c2;  // chunk: page c / 4, quarter c % 4
+      const int j = c >> 2, i = c & 3;
+      const char* src = k_lane + uint64_t(uint32_t(ids[j])) * page_bytes + i * 1024;
+      const uint32_t dst = __builtin_amdgcn_readfirstlane(
+          uint32_t(reinterpret_cast<uintptr_t>(&kst(stage_tag)[j][i * 64])));
+      asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
+                   :
+                   : "s"(dst), "v"(src)
+                   : "memory", "m0");
     }
+  };
+  auto stash = [&](int step, const uint4 (&r)[2]) {
+    const int t = elem >> 6, ln = elem & 63;
+    *reinterpret_cast<uint4*>(&ldv[step & 3][vpair][t][0][ln][0]) =
+        make_uint4(r[0].x, r[0].y, r[1].x, r[1].y);
+    *reinterpret_cast<uint4*>(&ldv[step & 3][vpair][t][1][ln][0]) =
+        make_uint4(r[0].z, r[0].w, r[1].z, r[1].w);
   };
 
   // Stage the page ids once (padded to whole steps with the last id), so that each
@@ -180,10 +226,10 @@ void chunk_kernel(ChunkArgs A) {
   __syncthreads();
 
   // Scores S^T = K . Q^T of page j of a stage, both column blocks.
-  auto qk_page = [&](int buf, int j, f32x4 (&sj)[kNB]) {
+  auto qk_page = [&](auto stage_tag, int j, f32x4 (&sj)[kNB]) {
     uint4 kr[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) kr[i] = ldk[buf][j][i * 64 + lane];
+    for (int i = 0; i < 4; ++i) kr[i] = kst(stage_tag)[j][i * 64 + lane];
 #pragma unroll
     for (int nb = 0; nb < kNB; ++nb) {
       f32x4 a = {0.f, 0.f, 0.f, 0.f};
@@ -233,7 +279,7 @@ void chunk_kernel(ChunkArgs A) {
   // from stage vbuf.  Exps of one pair overlap the previous pair's PV and this pair's
   // score MFMAs.  On the last step, V of slots at or past kv1 (never written, possibly
   // NaN) is zeroed in the operands.
-  auto pair = [&](int h, int kbuf, int vbuf, int key0, f32x4 (&s)[kStepPages][kNB],
+  auto pair = [&](int h, auto kstage_tag, int vbuf, int key0, f32x4 (&s)[kStepPages][kNB],
                   const float (&neg_m)[kNB], auto last_tag) {
     constexpr bool kLast = decltype(last_tag)::value;
     bf16x8 pop[kNB];
@@ -254,8 +300,8 @@ void chunk_kernel(ChunkArgs A) {
       pop[nb] = as_bf16x8(pb);
     }
     if constexpr (!kLast) {
-      qk_page(kbuf, 2 * h, s[2 * h]);
-      qk_page(kbuf, 2 * h + 1, s[2 * h + 1]);
+      qk_page(kstage_tag, 2 * h, s[2 * h]);
+      qk_page(kstage_tag, 2 * h + 1, s[2 * h + 1]);
     }
     uint4 vo[8];
 #pragma unroll
@@ -290,61 +336,77 @@ void chunk_kernel(ChunkArgs A) {
   // Staging registers come in two sets: step n + 3 is loaded into one while step n + 2,
   // loaded a whole step earlier, waits in the other to be written to LDS at the end of
   // step n, so each load has two steps of compute to land.
-  uint4 stage_a[kStepPages], stage_b[kStepPages];
+  uint4 stage_a[2], stage_b[2];
   if (nsteps > 0) {
-    fetch(0, stage_a);
+    copy_k(0, S0{});
+    fetch_v(0, stage_a);
     stash(0, stage_a);
   }
   if (nsteps > 1) {
-    fetch(1, stage_a);
+    copy_k(1, S1{});
+    fetch_v(1, stage_a);
     stash(1, stage_a);
   }
-  // Every load issued so far (Q operands, the first stages) has landed: the loop's
-  // wait counts then only track the in-loop prefetch.
+  if (nsteps > 2) copy_k(2, S2{});
+  // Every load issued so far (Q operands, the first stages, the direct K copies) has
+  // landed: the loop's wait counts then only track the in-loop prefetch.
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
-  if (nsteps > 2) fetch(2, stage_a);
+  if (nsteps > 2) fetch_v(2, stage_a);
 
   // One score set: each page's scores are replaced by the next step's as soon as its
   // probabilities are taken.
   f32x4 sc[kStepPages][kNB];
   if (nsteps > 0)
 #pragma unroll
-    for (int j = 0; j < kStepPages; ++j) qk_page(0, j, sc[j]);
-  // Every step before the last: no V tail to clear.  `landing` holds step n + 2,
-  // `flying` receives step n + 3; the staging sets swap roles every step.
-  using Stage = uint4[kStepPages];
-  // `buf` is n % kBufs, carried rather than recomputed.
-  auto next_buf = [](int buf) { return buf == kBufs - 1 ? 0 : buf + 1; };
-  auto step = [&](int n, int buf, Stage& landing, Stage& flying) {
+    for (int j = 0; j < kStepPages; ++j) qk_page(S0{}, j, sc[j]);
+  // Every step before the last: no V tail to clear.  `landing` holds V of step n + 2,
+  // `flying` receives V of step n + 3; the staging sets swap roles every step.  Step n
+  // starts the K copy of step n + 3 (into stage n + 3, last read in step n - 2) and
+  // loads V of step n + 3 between its two page pairs.  Before the closing barrier, at
+  // most the two V loads of step n + 3 may still be in flight: every older load (K of
+  // step n + 3 and everything of step n + 2) has landed: vmcnt(2) (vmcnt bits 3:0, expcnt
+  // 6:4 and lgkmcnt 11:8 left open).  The step index modulo 4 is a compile-time tag, so
+  // every K stage is a fixed array.
+  using Stage = uint4[2];
+  auto step = [&](int n, auto r_tag, Stage& landing, Stage& flying) {
+    constexpr int r = decltype(r_tag)::value;  // n & 3
+    using KRead = std::integral_constant<int, (r + 1) & 3>;
+    using KCopy = std::integral_constant<int, (r + 3) & 3>;
     const int key0 = n * kStepPages * kPage;
-    const int buf1 = next_buf(buf), buf2 = next_buf(buf1);
+    // Unconditional (past the end it re-loads the final step's pages, unused, into
+    // stages no one reads any more), so that the waits count the same loads every step.
+    copy_k(min(n + 3, nsteps - 1), KCopy{});
     float neg_m[kNB];
     prepare(key0, sc, neg_m);
-    pair(0, buf1, buf, key0, sc, neg_m, std::false_type{});
-    // Unconditional (the last steps re-load the final step's pages, unused), so that the
-    // wait before the stash below only ever counts this step's four loads as younger.
-    fetch(min(n + 3, nsteps - 1), flying);
-    pair(1, buf1, buf, key0, sc, neg_m, std::false_type{});
-    if (n + 2 < nsteps) stash(buf2, landing);
+    pair(0, KRead{}, r, key0, sc, neg_m, std::false_type{});
+    fetch_v(min(n + 3, nsteps - 1), flying);
+    pair(1, KRead{}, r, key0, sc, neg_m, std::false_type{});
+    if (n + 2 < nsteps) stash(n + 2, landing);
+    __builtin_amdgcn_s_waitcnt(0xF72);
     __syncthreads();
   };
-  int n0 = 0, buf0 = 0;
-  for (; n0 + 2 < nsteps; n0 += 2) {
-    step(n0, buf0, stage_a, stage_b);
-    step(n0 + 1, next_buf(buf0), stage_b, stage_a);
-    buf0 = next_buf(next_buf(buf0));
+  int n0 = 0;
+  for (; n0 + 4 < nsteps; n0 += 4) {
+    step(n0, S0{}, stage_a, stage_b);
+    step(n0 + 1, S1{}, stage_b, stage_a);
+    step(n0 + 2, S2{}, stage_a, stage_b);
+    step(n0 + 3, S3{}, stage_b, stage_a);
   }
+  // Up to three more steps before the last (n0 is a multiple of 4 here).
   if (n0 + 1 < nsteps) {
-    step(n0, buf0, stage_a, stage_b);
-    buf0 = next_buf(buf0);
+    step(n0, S0{}, stage_a, stage_b);
+    if (n0 + 2 < nsteps) {
+      step(n0 + 1, S1{}, stage_b, stage_a);
+      if (n0 + 3 < nsteps) step(n0 + 2, S2{}, stage_a, stage_b);
+    }
   }
   if (nsteps > 0) {
     const int key0 = (nsteps - 1) * kStepPages * kPage;
     float neg_m[kNB];
     prepare(key0, sc, neg_m);
-    pair(0, 0, buf0, key0, sc, neg_m, std::true_type{});
-    pair(1, 0, buf0, key0, sc, neg_m, std::true_type{});
+    pair(0, S0{}, (nsteps - 1) & 3, key0, sc, neg_m, std::true_type{});
+    pair(1, S0{}, (nsteps - 1) & 3, key0, sc, neg_m, std::true_type{});
   }
 
   // Epilogue: every column is owned by one wave; normalise and store.
