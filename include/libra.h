@@ -288,6 +288,14 @@ void libra_plan_destroy(libra_plan plan);
  * libra_plan_workspace_bytes(plan) bytes, 256-byte aligned.  `scale` must be finite.
  * Split rows write float32 partials; a second launch on the same stream merges them by
  * their log-sum-exps.
+ *
+ * HIP graphs: once the workspace holds the plan's tables (libra_plan_upload, or an
+ * earlier call of the plan on that workspace), a decode or append call only enqueues
+ * kernels (no allocation, host copy, memset or event), so it may be captured into a
+ * HIP graph.  The graph keeps the workspace, buffers and layout pointers it was
+ * captured with; while it may still be replayed, no other plan may use that workspace
+ * (its upload would replace the tables the graph's kernels read).  Per-kernel timing
+ * (libra_profile_enable) must be off during capture.
  */
 libra_status libra_decode_attn(libra_kv_layout layout, libra_plan plan, const void* q,
                                const int32_t* block_table, int32_t bt_stride, int32_t batch,
