@@ -75,8 +75,12 @@ def kernel_source_sha(kernel: str = "decode_kernel") -> str:
 
 
 def plan_sha(units: np.ndarray) -> str:
-    """Hash of a plan's unit table: a kernel's traffic depends on it (partials, tiles)."""
-    return hashlib.sha256(np.ascontiguousarray(units, dtype=np.int32).tobytes()).hexdigest()[:16]
+    """Hash of the set of a plan's units: a kernel's traffic depends on which units run
+    (their pages, partials and tiles), not on their order, which the slot placement of a
+    one-wave plan sets from measured XCD weights that differ between devices."""
+    u = np.ascontiguousarray(units, dtype=np.int32).reshape(-1, 12)
+    u = u[np.lexsort(u.T[::-1])]
+    return hashlib.sha256(np.ascontiguousarray(u).tobytes()).hexdigest()[:16]
 
 
 def traffic_from_profile(kernel: str, workload: str, units_sha: str):
@@ -559,6 +563,9 @@ def main():
     ap.add_argument("--units-per-cu", type=int, default=3)
     ap.add_argument("--min-split-pages", type=int, default=16)
     ap.add_argument("--max-splits", type=int, default=64)
+    ap.add_argument("--xcd-weights", default="measure",
+                    help="plan's per-XCD weights: 'measure' (libra_xcd_read_weights on the "
+                         "flush buffer), 'equal', or 8 comma-separated integers")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--copy-calibration", action="store_true",
@@ -631,8 +638,16 @@ def main():
 
     mode = libra.LIBRA_MODE_APPEND if w.append else libra.LIBRA_MODE_DECODE
     ql = batch.q_lens.tolist() if w.append else None
+    flush = torch.empty(args.flush_mib * (1 << 20) // 4, dtype=torch.float32, device=dev)
+    if args.xcd_weights == "measure":
+        xcd_weight = libra.libra_xcd_read_weights(flush, reps=10, stream=torch.cuda.current_stream())
+        log(f"[bench] measured XCD read weights {xcd_weight}")
+    elif args.xcd_weights == "equal":
+        xcd_weight = [0] * 8
+    else:
+        xcd_weight = [int(x) for x in args.xcd_weights.split(",")]
     plan_kw = dict(units_per_cu=args.units_per_cu, min_split_pages=args.min_split_pages,
-                   max_splits=args.max_splits)
+                   max_splits=args.max_splits, xcd_weight=xcd_weight)
     plan_times = []
     for _ in range(5):
         t = time.perf_counter()
@@ -655,7 +670,6 @@ def main():
             libra.libra_decode_attn(layout, plan, q, bt, bt.shape[1], len(batch.seq_lens),
                                     w.num_q_heads, batch.scale, ws, out, lse, stream=stream)
 
-    flush = torch.empty(args.flush_mib * (1 << 20) // 4, dtype=torch.float32, device=dev)
     log(f"[bench] warmup {args.warmup}")
     for i in range(args.warmup):
         flush.fill_(float(i))

@@ -213,6 +213,15 @@ libra_status libra_kv_reshard_host(const void* const* src, int32_t n_src, int32_
  *    on workgroups w with w % 8 = x, so the tiles of a part share an L2).
  * 10. Single rows with n_b > 1 own n_b float32 partial-result slots per KV head,
  *    allotted in ascending (b, g): part_base(b, g) = earlier split rows' slots + g n_b.
+ * 11. When step 4 decided (one wave of decode workgroups), the single units are placed
+ *    on compute-unit slots: the launch dispatches workgroup w to XCD w mod 8 and, all
+ *    units being resident at once, workgroups w, w + num_cus, w + 2 num_cus, ... to one
+ *    CU.  With n single units, slot c (0 <= c < num_cus) holds the positions w < n with
+ *    w mod num_cus = c and has weight x_c = xcd_weight[c mod 8] (1000 for 0).  A unit
+ *    costs the pages it reads, ceil(kv_end / 16) - floor(kv_begin / 16).  In step 9's
+ *    order, each unit goes to the slot with room that minimises (load_c + cost) / x_c
+ *    (exact cross-multiplied comparison, ties to the smaller c); the r-th unit a slot
+ *    receives is listed at position c + r num_cus.  Chunk-rule plans keep step 9's order.
  *
  * Unit fields (LIBRA_UNIT_INTS int32): b, g, kv_begin, kv_end, q_begin, q_end, split,
  * n_splits, part_base (-1 if unsplit), row0 (first query row of sequence b),
@@ -225,6 +234,9 @@ typedef struct libra_plan_params {
   int32_t min_split_pages;  /* default 16 */
   int32_t max_splits;       /* default 64 */
   int32_t q_tile;           /* chunk query tile in tokens, at most floor(256 / G); 0 = that */
+  int32_t xcd_weight[8];    /* step 11: relative HBM read rate of the CUs of XCD x, in
+                               [1, 1000000]; 0 = 1000 (all equal when every entry is 0).
+                               libra_xcd_read_weights measures it. */
 } libra_plan_params;
 
 typedef struct libra_plan_desc {
@@ -254,6 +266,19 @@ typedef struct libra_plan_info {
 libra_status libra_splitkv_plan(const libra_plan_desc* desc, const int32_t* seq_lens_host,
                                 const int32_t* q_lens_host, const libra_plan_params* params,
                                 libra_plan* out);
+/* Measures the xcd_weight plan parameter on the current device.  With every CU
+ * reading at once, the XCDs of one device may get unequal shares of HBM bandwidth, and
+ * a one-wave decode launch then ends when the slowest XCD does.  2048 workgroups of 256
+ * threads each stream one equal, contiguous block of `buf` (device memory of any
+ * contents, 256-byte aligned, bytes >= 64 MiB; only read) with 16-byte non-temporal
+ * loads and record when they finish and on which XCD they ran; this runs reps + 1 times
+ * (1 <= reps <= 100), the first run not counted.  weights[x] (8 entries, host) =
+ * round(1000 * F / T_x), T_x being XCD x's mean finish time over its workgroups and
+ * runs and F the smallest T_x, clamped to [1, 1000]; an XCD that ran no workgroup gets
+ * 0 (the plan's default).  Allocates 64 KiB of device memory for the call and waits for
+ * `stream`: for set-up, not for graph capture. */
+libra_status libra_xcd_read_weights(const void* buf, size_t bytes, int32_t reps,
+                                    int32_t* weights, void* stream);
 /* Host view of the unit table (valid until libra_plan_destroy). */
 libra_status libra_plan_get_units(libra_plan plan, const int32_t** units_host, int32_t* n_units);
 libra_status libra_plan_get_info(libra_plan plan, libra_plan_info* info);

@@ -52,6 +52,14 @@ units per CU, minimum split size in pages, maximum splits, chunk query tile).
 10. Single rows with n_b > 1 own n_b partial-result slots per KV head, allotted in
     ascending (b, g) order: part_base(b, g) = (slots of earlier split rows) + g * n_b.
     Units with n_b = 1 have part_base = -1.
+11. When step 4 decided, the single units are placed on compute-unit slots (the decode
+    launch puts workgroup w on XCD w mod 8 and, with every unit resident at once,
+    workgroups w, w + num_cus, ... on one CU).  With n single units, slot c holds the
+    positions w < n with w mod num_cus = c; its weight is xcd_weight[c mod 8] (1000 for
+    0).  A unit costs ceil(kv_end / 16) - floor(kv_begin / 16) pages.  Taking the units
+    in step 9's order, each goes to the slot with room whose (load + cost) / weight is
+    smallest (exact comparison, ties to the smaller c); the r-th unit of slot c is listed
+    at position c + r * num_cus.
 
 Each unit is 12 int32 fields, in the order of ``UNIT_FIELDS``.
 """
@@ -74,6 +82,7 @@ class PlanParams:
     min_split_pages: int = 16
     max_splits: int = 64
     q_tile: int = 0
+    xcd_weight: tuple = (0, 0, 0, 0, 0, 0, 0, 0)
 
 
 def _ceil_div(a: int, b: int) -> int:
@@ -110,6 +119,33 @@ def _one_wave_splits(pages, single, R, params):
     if 2 * largest * R > 3 * sum(pages[b] for b in single):
         return None
     return n
+
+
+def _place_on_slots(units, params):
+    """Step 11: deal the units to compute-unit slots, each to the slot with room that
+    minimises (load + cost) / weight, scanning every slot."""
+    n, S = len(units), params.num_cus
+    weight = [x if x > 0 else 1000 for x in params.xcd_weight]
+    cap = [len(range(c, n, S)) for c in range(S)]
+    load = [0] * S
+    placed = [[] for _ in range(S)]
+    for u in units:
+        cost = _ceil_div(u[3], PAGE) - u[2] // PAGE
+        best = None
+        for c in range(S):
+            if len(placed[c]) == cap[c]:
+                continue
+            # (load_c + cost) / w_c < (load_best + cost) / w_best, cross-multiplied
+            if best is None or ((load[c] + cost) * weight[best % NUM_XCDS]
+                                < (load[best] + cost) * weight[c % NUM_XCDS]):
+                best = c
+        placed[best].append(u)
+        load[best] += cost
+    out = [None] * n
+    for c in range(S):
+        for r, u in enumerate(placed[c]):
+            out[c + r * S] = u
+    return out
 
 
 def plan_ref(seq_lens, q_lens, num_kv_heads: int, group: int, params: PlanParams):
@@ -159,6 +195,8 @@ def plan_ref(seq_lens, q_lens, num_kv_heads: int, group: int, params: PlanParams
                 singles.append((b, g, t0, t1, 0, 1, j, n, part_base.get((b, g), -1),
                                 row0[b], KIND_SINGLE, L[b] - 1))
     singles.sort(key=lambda u: (-(u[3] - u[2]), u[0], u[1], u[6]))
+    if balanced and singles:
+        singles = _place_on_slots(singles, params)
 
     T = params.q_tile if params.q_tile > 0 else 256 // group
     chunks = []

@@ -382,7 +382,7 @@ libra_status libra_splitkv_plan(const libra_plan_desc* desc, const int32_t* seq_
   if (d.mode == LIBRA_MODE_APPEND && d.batch > 0 && !q_lens_host)
     return set_error(LIBRA_E_INVAL, "append plans need q_lens_host");
 
-  libra_plan_params p{0, 3, 16, 64, 0};
+  libra_plan_params p{0, 3, 16, 64, 0, {0, 0, 0, 0, 0, 0, 0, 0}};
   if (params) p = *params;
   if (p.num_cus == 0) {
     int dev = 0, cus = 0;
@@ -394,6 +394,9 @@ libra_status libra_splitkv_plan(const libra_plan_desc* desc, const int32_t* seq_
   if (p.num_cus <= 0 || p.units_per_cu <= 0 || p.min_split_pages <= 0 || p.max_splits <= 0 ||
       p.q_tile < 0)
     return set_error(LIBRA_E_INVAL, "plan parameters must be positive");
+  for (int x = 0; x < kNumXcds; ++x)
+    if (p.xcd_weight[x] < 0 || p.xcd_weight[x] > 1000000)
+      return set_error(LIBRA_E_INVAL, "xcd_weight entries must lie in [0, 1000000]");
   if (p.q_tile > kChunkRows / G)
     return set_error(LIBRA_E_UNSUPPORTED, "q_tile larger than floor(256 / G) tokens");
 
@@ -412,6 +415,16 @@ libra_status libra_splitkv_plan(const libra_plan_desc* desc, const int32_t* seq_
   }
   *out = P;
   return LIBRA_OK;
+}
+
+libra_status libra_xcd_read_weights(const void* buf, size_t bytes, int32_t reps,
+                                    int32_t* weights, void* stream) {
+  if (!buf || !weights) return set_error(LIBRA_E_INVAL, "buf or weights is NULL");
+  if (reinterpret_cast<uintptr_t>(buf) % kWorkspaceAlign)
+    return set_error(LIBRA_E_INVAL, "buf must be 256-byte aligned");
+  if (bytes < (size_t(64) << 20)) return set_error(LIBRA_E_INVAL, "buf must hold at least 64 MiB");
+  if (reps < 1 || reps > 100) return set_error(LIBRA_E_INVAL, "reps must lie in [1, 100]");
+  return measure_xcd_weights(buf, bytes, reps, weights, static_cast<hipStream_t>(stream));
 }
 
 libra_status libra_plan_get_units(libra_plan plan, const int32_t** units_host, int32_t* n_units) {

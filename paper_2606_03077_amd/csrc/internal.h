@@ -68,6 +68,9 @@ hipError_t launch_page_copy(const KvLayout& L, const int32_t* ids, int64_t n, vo
                             void* v_run, bool to_run, hipStream_t s);
 hipError_t launch_merge(const Plan& P, void* ws, void* out, float* lse, hipStream_t s);
 bool merge_launches(const Plan& P);  // whether launch_merge enqueues a kernel for P
+// Streams buf (reps + 1 launches, the first not counted) and writes per-XCD weights.
+libra_status measure_xcd_weights(const void* buf, size_t bytes, int reps, int32_t* weights,
+                                 hipStream_t s);
 hipError_t launch_chunk(const KvLayout& L, const Plan& P, void* ws, const void* q,
                         const int32_t* bt, int32_t stride, float scale, void* out, float* lse,
                         hipStream_t s);

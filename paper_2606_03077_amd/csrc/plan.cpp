@@ -50,6 +50,46 @@ bool one_wave_splits(const std::vector<int64_t>& pages, const std::vector<int64_
   return true;
 }
 
+// Rule step 11: the units (in step 9's order) are dealt to compute-unit slots, each to
+// the slot with room that minimises (load + cost) / weight; the r-th unit of slot c is
+// listed at position c + r * num_cus.  Slots of one XCD share a weight, so one min-heap of
+// (load, c) per XCD yields that XCD's best slot and the eight candidates are compared
+// exactly; this picks the same slot as a scan over all of them.
+std::vector<Unit> place_on_slots(const std::vector<Unit>& units, const libra_plan_params& p) {
+  const int64_t n = int64_t(units.size()), S = p.num_cus;
+  auto weight = [&](int64_t c) -> int64_t {
+    const int32_t x = p.xcd_weight[c % kNumXcds];
+    return x > 0 ? x : 1000;
+  };
+  auto cap = [&](int64_t c) { return c < n ? (n - 1 - c) / S + 1 : int64_t(0); };
+  using Entry = std::pair<int64_t, int64_t>;  // (load, slot)
+  std::array<std::priority_queue<Entry, std::vector<Entry>, std::greater<Entry>>, kNumXcds> heaps;
+  for (int64_t c = 0; c < std::min(S, n); ++c) heaps[c % kNumXcds].push({0, c});
+  std::vector<int64_t> taken(size_t(std::min(S, n)), 0);
+  std::vector<Unit> out(units.size());
+  for (const Unit& u : units) {
+    const int64_t cost = ceil_div(u[U_KV1], kPage) - u[U_KV0] / kPage;
+    int best = -1;
+    Entry be{0, 0};
+    for (int k = 0; k < kNumXcds; ++k) {
+      if (heaps[k].empty()) continue;
+      const Entry e = heaps[k].top();
+      if (best >= 0) {
+        const __int128 lhs = __int128(e.first + cost) * weight(be.second);
+        const __int128 rhs = __int128(be.first + cost) * weight(e.second);
+        if (lhs > rhs || (lhs == rhs && e.second > be.second)) continue;
+      }
+      best = k;
+      be = e;
+    }
+    heaps[best].pop();
+    const int64_t c = be.second;
+    out[size_t(c + taken[c] * S)] = u;
+    if (++taken[c] < cap(c)) heaps[best].push({be.first + cost, c});
+  }
+  return out;
+}
+
 }  // namespace
 
 libra_status build_plan(const libra_plan_desc& d, const int32_t* seq_lens, const int32_t* q_lens,
@@ -132,6 +172,7 @@ libra_status build_plan(const libra_plan_desc& d, const int32_t* seq_lens, const
     if (x[U_G] != y[U_G]) return x[U_G] < y[U_G];
     return x[U_SPLIT] < y[U_SPLIT];
   });
+  if (balanced && !singles.empty()) singles = place_on_slots(singles, p);  // step 11
 
   // Step 7: query tiles of chunk rows.
   const int64_t T = p.q_tile > 0 ? p.q_tile : int64_t(kChunkRows) / G;

@@ -31,7 +31,8 @@ UNIT_FIELDS = ("b", "g", "kv_begin", "kv_end", "q_begin", "q_end", "split", "n_s
 EXPORTS = ("libra_status_string", "libra_last_error", "libra_kv_layout_create",
            "libra_kv_layout_destroy", "libra_kv_pack_pages", "libra_kv_unpack_pages",
            "libra_kv_gather", "libra_kv_copy_out", "libra_kv_copy_in", "libra_kv_reshard_host",
-           "libra_splitkv_plan", "libra_plan_get_units", "libra_plan_get_info",
+           "libra_xcd_read_weights", "libra_splitkv_plan", "libra_plan_get_units",
+           "libra_plan_get_info",
            "libra_plan_workspace_bytes", "libra_plan_upload", "libra_plan_destroy",
            "libra_decode_attn", "libra_append_attn", "libra_profile_enable",
            "libra_profile_collect", "libra_ce_fit", "libra_ce_mape", "libra_ce_poly_sum",
@@ -58,7 +59,7 @@ class LayoutDesc(ctypes.Structure):
 class PlanParams(ctypes.Structure):
     _fields_ = [("num_cus", ctypes.c_int32), ("units_per_cu", ctypes.c_int32),
                 ("min_split_pages", ctypes.c_int32), ("max_splits", ctypes.c_int32),
-                ("q_tile", ctypes.c_int32)]
+                ("q_tile", ctypes.c_int32), ("xcd_weight", ctypes.c_int32 * 8)]
 
 
 class PlanDesc(ctypes.Structure):
@@ -123,6 +124,7 @@ def load() -> ctypes.CDLL:
                                                  I32, I64]),
         "libra_splitkv_plan": (ctypes.c_int, [ctypes.POINTER(PlanDesc), I32P, I32P,
                                               ctypes.POINTER(PlanParams), ctypes.POINTER(P)]),
+        "libra_xcd_read_weights": (ctypes.c_int, [P, SZ, I32, I32P, P]),
         "libra_plan_get_units": (ctypes.c_int, [P, ctypes.POINTER(I32P), I32P]),
         "libra_plan_get_info": (ctypes.c_int, [P, ctypes.POINTER(PlanInfo)]),
         "libra_plan_workspace_bytes": (SZ, [P]),
@@ -282,9 +284,14 @@ def libra_kv_gather(layout: int, block_table, bt_stride: int, cu_seq_lens, batch
 def libra_splitkv_plan(mode: int, batch: int, num_q_heads: int, num_kv_heads: int,
                        seq_lens: Sequence[int], q_lens: Optional[Sequence[int]] = None,
                        num_cus: int = 0, units_per_cu: int = 3, min_split_pages: int = 16,
-                       max_splits: int = 64, q_tile: int = 0) -> int:
+                       max_splits: int = 64, q_tile: int = 0,
+                       xcd_weight: Optional[Sequence[int]] = None) -> int:
     d = PlanDesc(mode, batch, num_q_heads, num_kv_heads)
-    p = PlanParams(num_cus, units_per_cu, min_split_pages, max_splits, q_tile)
+    w = list(xcd_weight) if xcd_weight is not None else [0] * 8
+    if len(w) != 8:
+        raise ValueError("xcd_weight needs 8 entries")
+    p = PlanParams(num_cus, units_per_cu, min_split_pages, max_splits, q_tile,
+                   (ctypes.c_int32 * 8)(*w))
     sl = _i32_array(seq_lens)
     ql = None if q_lens is None else _i32_array(q_lens)
     I32P = ctypes.POINTER(ctypes.c_int32)
@@ -295,6 +302,15 @@ def libra_splitkv_plan(mode: int, batch: int, num_q_heads: int, num_kv_heads: in
                                      None if ql is None else ql.ctypes.data_as(I32P),
                                      ctypes.byref(p), ctypes.byref(h)), "libra_splitkv_plan")
     return h.value
+
+
+def libra_xcd_read_weights(buf, reps: int = 5, stream=None) -> list:
+    """Per-XCD HBM read weights measured by streaming the device buffer `buf` (>= 64 MiB)."""
+    w = (ctypes.c_int32 * 8)()
+    nbytes = buf.numel() * buf.element_size()
+    _check(load().libra_xcd_read_weights(_ptr(buf), nbytes, reps, w, _stream(stream)),
+           "libra_xcd_read_weights")
+    return list(w)
 
 
 def libra_plan_get_units(plan: int) -> np.ndarray:

@@ -44,6 +44,7 @@ int main() {
     const int tpb = G >= 16 ? 1 : 16 / G;
     libra_plan_params p{int32_t(uni(1, 512)), int32_t(uni(1, 8)), int32_t(uni(1, 64)),
                         int32_t(uni(1, 128)), int32_t(uni(0, 1) ? 0 : uni(1, 16 * tpb))};
+    for (int x = 0; x < 8; ++x) p.xcd_weight[x] = int32_t(uni(0, 3) == 0 ? 0 : uni(1, 1000000));
     libra_plan plan = nullptr;
     const libra_status st = libra_splitkv_plan(&d, L.data(), append ? C.data() : nullptr, &p, &plan);
     if (st != LIBRA_OK) continue;
@@ -56,6 +57,8 @@ int main() {
     int64_t sum = 0;
     for (int i = 0; i < n; ++i) sum ^= units[i * LIBRA_UNIT_INTS + 3];
     (void)sum;
+    for (int i = 0; i < info.n_single; ++i)  // every slot position holds a real unit
+      CHECK(units[i * LIBRA_UNIT_INTS + 7] >= 1 && units[i * LIBRA_UNIT_INTS + 10] == 0);
     CHECK(libra_plan_workspace_bytes(plan) >= 256);
     libra_plan_destroy(plan);
   }

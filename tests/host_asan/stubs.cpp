@@ -11,5 +11,6 @@ hipError_t launch_decode(const KvLayout&, const Plan&, void*, const void*, const
 hipError_t launch_merge(const Plan&, void*, void*, float*, hipStream_t) { return hipErrorUnknown; }
 bool merge_launches(const Plan&) { return false; }
 hipError_t launch_chunk(const KvLayout&, const Plan&, void*, const void*, const int32_t*, int32_t, float, void*, float*, hipStream_t) { return hipErrorUnknown; }
+libra_status measure_xcd_weights(const void*, size_t, int, int32_t*, hipStream_t) { return LIBRA_E_HIP; }
 hipError_t launch_page_copy(const KvLayout&, const int32_t*, int64_t, void*, void*, bool, hipStream_t) { return hipErrorUnknown; }
 }  // namespace libra

@@ -47,7 +47,7 @@ def test_status_strings():
 def _plan_units(mode, B, hq, hkv, lens, qlens, params):
     h = libra.libra_splitkv_plan(mode, B, hq, hkv, lens, qlens, params.num_cus,
                                  params.units_per_cu, params.min_split_pages, params.max_splits,
-                                 params.q_tile)
+                                 params.q_tile, list(params.xcd_weight))
     try:
         return libra.libra_plan_get_units(h), libra.libra_plan_get_info(h)
     finally:
@@ -72,8 +72,10 @@ def test_plan_bit_exact_on_workload_lengths(name):
     w = wl.WORKLOADS[name]
     lens, qlens = wl.draw_lengths(w, np.random.default_rng(w.seed))
     q = qlens.tolist() if w.append else None
+    odd_slow = (1000, 910, 1000, 910, 1000, 910, 1000, 910)
     for params in [oracle.PlanParams(), oracle.PlanParams(num_cus=256, units_per_cu=3,
-                                                          min_split_pages=8, max_splits=128)]:
+                                                          min_split_pages=8, max_splits=128),
+                   oracle.PlanParams(xcd_weight=odd_slow)]:
         _compare(lens.tolist(), q, w.num_q_heads, w.num_kv_heads, params)
 
 
@@ -100,9 +102,13 @@ def _one_wave_case(seed):
     hkv = int(rng.choice([1, 2, 4, 8]))
     upc = int(rng.integers(1, 5))
     waves = float(rng.choice([1.0, 1.5, 3.0, 6.0]))   # budget R relative to the row count
+    weights = [int(rng.choice([0, 1, 500, 910, 1000, 1000000])) for _ in range(8)]
+    if seed % 3 == 0:
+        weights = [0] * 8
     params = oracle.PlanParams(num_cus=int(np.ceil(waves * B * hkv / upc)), units_per_cu=upc,
                                min_split_pages=int(rng.choice([1, 4, 16])),
-                               max_splits=int(rng.choice([3, 16, 64, 64])))
+                               max_splits=int(rng.choice([3, 16, 64, 64])),
+                               xcd_weight=tuple(weights))
     return _compare(lens.astype(int).tolist(), None, 4 * hkv, hkv, params)["balanced"]
 
 
@@ -150,9 +156,27 @@ def test_plan_validation_codes():
     assert _status_of(P, D, 1, 8, 2, [-1], None, 8) == 1            # negative length
     assert _status_of(P, D, 1, 8, 2, [5], None, 8, 0) == 1          # units_per_cu = 0
     assert _status_of(P, A, 1, 8, 2, [90], [80], 8, 2, 32, 64, 65) == 2  # q_tile > 256 / 4
+    assert _status_of(P, D, 1, 8, 2, [5], None, 8, 3, 16, 64, 0, [0] * 7 + [-1]) == 1
+    assert _status_of(P, D, 1, 8, 2, [5], None, 8, 3, 16, 64, 0, [1000001] + [0] * 7) == 1
+    h = P(D, 1, 8, 2, [5], None, 8, 3, 16, 64, 0, [1000000] * 8)      # weights at the limit
+    libra.libra_plan_destroy(h)
     h = P(D, 0, 8, 2, [], None, 8)                                    # empty batch is valid
     assert libra.libra_plan_get_info(h)["n_units"] == 0
     libra.libra_plan_destroy(h)
+
+
+def test_xcd_read_weights_validation_codes():
+    # Argument checks come before any HIP call (fake device addresses are never touched).
+    lib = libra.load()
+    w = (ctypes.c_int32 * 8)()
+    fake, mib = 1 << 30, 1 << 20
+    call = lambda buf, nbytes, reps, out=w: lib.libra_xcd_read_weights(buf, nbytes, reps, out, None)
+    assert call(None, 64 * mib, 1) == 1                 # NULL buffer
+    assert call(fake, 64 * mib, 1, None) == 1           # NULL weights
+    assert call(fake + 16, 64 * mib, 1) == 1            # not 256-byte aligned
+    assert call(fake, 64 * mib - 1, 1) == 1             # smaller than 64 MiB
+    assert call(fake, 64 * mib, 0) == 1                 # reps < 1
+    assert call(fake, 64 * mib, 101) == 1               # reps > 100
 
 
 def test_layout_validation_codes():

@@ -1,4 +1,6 @@
 """Pins for the plan oracle: hand-derived tables and the invariants the rule promises."""
+import dataclasses
+
 import numpy as np
 import pytest
 
@@ -77,6 +79,71 @@ def test_few_groups_fill_every_queue():
     assert max(qcost) - min(qcost) <= 0.02 * sum(cost)
 
 
+def check_slot_placement(singles, params):
+    """Step 11 read off the output: position w belongs to slot w % num_cus; slot c holds
+    exactly the positions w < n with w % num_cus = c; replaying the units in step 9's
+    order (descending KV tokens, ties (b, g, j)), each unit's slot had room and no slot
+    with room had a smaller (load + cost) / weight, nor an equal one with a smaller
+    index; and a slot's units keep step 9's order across its positions."""
+    from fractions import Fraction
+    n, S = len(singles), params.num_cus
+    w8 = [x if x > 0 else 1000 for x in params.xcd_weight]
+    slot_of = {}
+    for w, u in enumerate(singles):
+        slot_of.setdefault(u, []).append(w % S)
+    order = sorted(singles, key=lambda u: (-(u[3] - u[2]), u[0], u[1], u[6]))
+    cap = [len(range(c, n, S)) for c in range(S)]
+    load, used, seq = [0] * S, [0] * S, [[] for _ in range(S)]
+    for u in order:
+        c = slot_of[u].pop(0)
+        cost = -(-u[3] // 16) - u[2] // 16
+        assert used[c] < cap[c]
+        mine = Fraction(load[c] + cost, w8[c % 8])
+        for d in range(S):
+            if used[d] < cap[d]:
+                other = Fraction(load[d] + cost, w8[d % 8])
+                assert other > mine or (other == mine and d >= c), (u, c, d)
+        load[c] += cost
+        used[c] += 1
+        seq[c].append(u)
+    assert used == cap
+    for c in range(S):
+        assert [singles[w] for w in range(c, n, S)] == seq[c]
+
+
+def test_hand_derived_slot_placement():
+    # Six one-page-multiple rows, Hkv = 1, 2 CUs x 3 units: S = 6 = R, so step 4 keeps one
+    # split each (pages 6, 5, 5, 4, 4, 3; 2 * 6 * 6 = 72 <= 3 * 27 = 81: balanced) and
+    # step 9 lists b = 0..5.  Equal weights: 6 -> slot 0; 5 -> slot 1; 5 -> slot 1 (5 + 5
+    # = 10 < 6 + 5); 4 -> slot 0 (10 < 14); 4 -> tie at 14, slot 0 (now full); 3 -> slot
+    # 1.  Slot 0 holds b0, b3, b4 at positions 0, 2, 4, slot 1 holds b1, b2, b5 at 1, 3, 5.
+    lens = [96, 80, 80, 64, 64, 48]
+    unit = lambda b: (b, 0, 0, lens[b], 0, 1, 0, 1, -1, b, 0, lens[b] - 1)
+    par = dict(num_cus=2, units_per_cu=3, min_split_pages=1)
+    units, info = plan_ref(lens, None, 1, 4, PlanParams(**par))
+    assert info["balanced"]
+    assert units == [unit(b) for b in (0, 1, 3, 2, 4, 5)]
+    # Slot 1 at half speed (weight 500): 6 -> slot 0 (6/1000 < 6/500); 5 -> slot 1
+    # (5/500 = 0.010 < 11/1000); 5 -> slot 0 (11/1000 < 10/500); 4 -> slot 0 (15/1000 <
+    # 9/500), which is then full; 4 and 3 -> slot 1.  Slot 0: b0, b2, b3; slot 1: b1, b4, b5.
+    units, _ = plan_ref(lens, None, 1, 4, PlanParams(**par, xcd_weight=(1000, 500, 0, 0, 0, 0, 0, 0)))
+    assert units == [unit(b) for b in (0, 1, 2, 4, 3, 5)]
+
+
+def test_slot_placement_catches_a_planted_mistake(monkeypatch):
+    # A placement that ignores the weights breaks the replay check.
+    import oracle.plan as op
+    lens = [96, 80, 80, 64, 64, 48]
+    params = PlanParams(num_cus=2, units_per_cu=3, min_split_pages=1,
+                        xcd_weight=(1000, 500, 0, 0, 0, 0, 0, 0))
+    real = op._place_on_slots
+    monkeypatch.setattr(op, "_place_on_slots",
+                        lambda units, p: real(units, dataclasses.replace(p, xcd_weight=(0,) * 8)))
+    units, _ = op.plan_ref(lens, None, 1, 4, params)
+    with pytest.raises(AssertionError):
+        check_slot_placement(units, params)
+
+
 def check_invariants(seq_lens, q_lens, hkv, group, params):
     units, info = plan_ref(seq_lens, q_lens, hkv, group, params)
     B = len(seq_lens)
@@ -84,9 +151,12 @@ def check_invariants(seq_lens, q_lens, hkv, group, params):
     singles = units[:info["n_single"]]
     chunks = units[info["n_single"]:]
     assert all(u[F["kind"]] == 0 for u in singles) and all(u[F["kind"]] == 1 for u in chunks)
-    # ordering
+    # ordering: step 9's descending KV order, or in a one-wave plan step 11's slots
     kv = [u[3] - u[2] for u in singles]
-    assert kv == sorted(kv, reverse=True)
+    if info["balanced"] and singles:
+        check_slot_placement(singles, params)
+    else:
+        assert kv == sorted(kv, reverse=True)
     # chunk units: per-XCD queues, each (b, g) group contiguous inside one queue with its
     # tiles by descending cost, groups dealt to the least-loaded queue
     cost = lambda u: (u[3] - u[2]) * (u[5] - u[4])
