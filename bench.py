@@ -640,7 +640,9 @@ def main():
     ql = batch.q_lens.tolist() if w.append else None
     flush = torch.empty(args.flush_mib * (1 << 20) // 4, dtype=torch.float32, device=dev)
     if args.xcd_weights == "measure":
-        xcd_weight = libra.libra_xcd_read_weights(flush, reps=10, stream=torch.cuda.current_stream())
+        calib = flush if flush.numel() * 4 >= (1 << 30) else torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        xcd_weight = libra.libra_xcd_read_weights(calib, reps=10, stream=torch.cuda.current_stream())
+        del calib
         log(f"[bench] measured XCD read weights {xcd_weight}")
     elif args.xcd_weights == "equal":
         xcd_weight = [0] * 8

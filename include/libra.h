@@ -213,15 +213,16 @@ libra_status libra_kv_reshard_host(const void* const* src, int32_t n_src, int32_
  *    on workgroups w with w % 8 = x, so the tiles of a part share an L2).
  * 10. Single rows with n_b > 1 own n_b float32 partial-result slots per KV head,
  *    allotted in ascending (b, g): part_base(b, g) = earlier split rows' slots + g n_b.
- * 11. When step 4 decided (one wave of decode workgroups), the single units are placed
- *    on compute-unit slots: the launch dispatches workgroup w to XCD w mod 8 and, all
- *    units being resident at once, workgroups w, w + num_cus, w + 2 num_cus, ... to one
- *    CU.  With n single units, slot c (0 <= c < num_cus) holds the positions w < n with
- *    w mod num_cus = c and has weight x_c = xcd_weight[c mod 8] (1000 for 0).  A unit
- *    costs the pages it reads, ceil(kv_end / 16) - floor(kv_begin / 16).  In step 9's
- *    order, each unit goes to the slot with room that minimises (load_c + cost) / x_c
- *    (exact cross-multiplied comparison, ties to the smaller c); the r-th unit a slot
- *    receives is listed at position c + r num_cus.  Chunk-rule plans keep step 9's order.
+ * 11. The single units are placed on S slots.  The decode launch dispatches workgroup w
+ *    to XCD w mod 8; when step 4 decided, all units are resident at once and workgroups
+ *    w, w + num_cus, w + 2 num_cus, ... share one CU, so S = num_cus (CU slots);
+ *    otherwise each XCD runs its workgroups as its CUs free up, so S = 8 (XCD queues).
+ *    With n single units, slot c (0 <= c < S) holds the positions w < n with w mod S = c
+ *    and has weight x_c = xcd_weight[c mod 8] (1000 for 0).  A unit costs the pages it
+ *    reads, ceil(kv_end / 16) - floor(kv_begin / 16).  In step 9's order, each unit goes
+ *    to the slot with room that minimises (load_c + cost) / x_c (exact cross-multiplied
+ *    comparison, ties to the smaller c); the r-th unit a slot receives is listed at
+ *    position c + r S.
  *
  * Unit fields (LIBRA_UNIT_INTS int32): b, g, kv_begin, kv_end, q_begin, q_end, split,
  * n_splits, part_base (-1 if unsplit), row0 (first query row of sequence b),
@@ -267,16 +268,16 @@ libra_status libra_splitkv_plan(const libra_plan_desc* desc, const int32_t* seq_
                                 const int32_t* q_lens_host, const libra_plan_params* params,
                                 libra_plan* out);
 /* Measures the xcd_weight plan parameter on the current device.  With every CU
- * reading at once, the XCDs of one device may get unequal shares of HBM bandwidth, and
- * a one-wave decode launch then ends when the slowest XCD does.  2048 workgroups of 256
- * threads each stream one equal, contiguous block of `buf` (device memory of any
- * contents, 256-byte aligned, bytes >= 64 MiB; only read) with 16-byte non-temporal
- * loads and record when they finish and on which XCD they ran; this runs reps + 1 times
- * (1 <= reps <= 100), the first run not counted.  weights[x] (8 entries, host) =
- * round(1000 * F / T_x), T_x being XCD x's mean finish time over its workgroups and
- * runs and F the smallest T_x, clamped to [1, 1000]; an XCD that ran no workgroup gets
- * 0 (the plan's default).  Allocates 64 KiB of device memory for the call and waits for
- * `stream`: for set-up, not for graph capture. */
+ * reading at once, the XCDs of one device may get unequal shares of HBM bandwidth, and a
+ * decode launch then ends when the slowest XCD does.  2048 workgroups of 256 threads each
+ * stream their own contiguous block of `buf` (device memory of any contents, 256-byte
+ * aligned, bytes >= 1 GiB so that no block is read twice; only read) with 16-byte
+ * non-temporal loads for 100 us of the device's constant clock and count the loads they
+ * issue, per XCD; this runs reps + 1 times (1 <= reps <= 100), the first run not counted.
+ * weights[x] (8 entries, host) = round(1000 * N_x / max_y N_y), N_x being the loads
+ * issued on XCD x over the counted runs, clamped to [1, 1000]; an XCD that ran no
+ * workgroup gets 0 (the plan's default).  Allocates 64 KiB of device memory for the call
+ * and waits for `stream`: for set-up, not for graph capture. */
 libra_status libra_xcd_read_weights(const void* buf, size_t bytes, int32_t reps,
                                     int32_t* weights, void* stream);
 /* Host view of the unit table (valid until libra_plan_destroy). */

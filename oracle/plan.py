@@ -52,14 +52,15 @@ units per CU, minimum split size in pages, maximum splits, chunk query tile).
 10. Single rows with n_b > 1 own n_b partial-result slots per KV head, allotted in
     ascending (b, g) order: part_base(b, g) = (slots of earlier split rows) + g * n_b.
     Units with n_b = 1 have part_base = -1.
-11. When step 4 decided, the single units are placed on compute-unit slots (the decode
-    launch puts workgroup w on XCD w mod 8 and, with every unit resident at once,
-    workgroups w, w + num_cus, ... on one CU).  With n single units, slot c holds the
-    positions w < n with w mod num_cus = c; its weight is xcd_weight[c mod 8] (1000 for
-    0).  A unit costs ceil(kv_end / 16) - floor(kv_begin / 16) pages.  Taking the units
-    in step 9's order, each goes to the slot with room whose (load + cost) / weight is
-    smallest (exact comparison, ties to the smaller c); the r-th unit of slot c is listed
-    at position c + r * num_cus.
+11. The single units are placed on S slots.  The decode launch puts workgroup w on XCD
+    w mod 8; when step 4 decided, every unit is resident at once and workgroups w,
+    w + num_cus, ... share one CU, so S = num_cus; otherwise each XCD runs its workgroups
+    as its CUs free up, so S = 8.  With n single units, slot c holds the positions w < n
+    with w mod S = c; its weight is xcd_weight[c mod 8] (1000 for 0).  A unit costs
+    ceil(kv_end / 16) - floor(kv_begin / 16) pages.  Taking the units in step 9's order,
+    each goes to the slot with room whose (load + cost) / weight is smallest (exact
+    comparison, ties to the smaller c); the r-th unit of slot c is listed at position
+    c + r * S.
 
 Each unit is 12 int32 fields, in the order of ``UNIT_FIELDS``.
 """
@@ -121,10 +122,10 @@ def _one_wave_splits(pages, single, R, params):
     return n
 
 
-def _place_on_slots(units, params):
-    """Step 11: deal the units to compute-unit slots, each to the slot with room that
-    minimises (load + cost) / weight, scanning every slot."""
-    n, S = len(units), params.num_cus
+def _place_on_slots(units, params, S):
+    """Step 11: deal the units to S slots, each to the slot with room that minimises
+    (load + cost) / weight, scanning every slot."""
+    n = len(units)
     weight = [x if x > 0 else 1000 for x in params.xcd_weight]
     cap = [len(range(c, n, S)) for c in range(S)]
     load = [0] * S
@@ -195,8 +196,8 @@ def plan_ref(seq_lens, q_lens, num_kv_heads: int, group: int, params: PlanParams
                 singles.append((b, g, t0, t1, 0, 1, j, n, part_base.get((b, g), -1),
                                 row0[b], KIND_SINGLE, L[b] - 1))
     singles.sort(key=lambda u: (-(u[3] - u[2]), u[0], u[1], u[6]))
-    if balanced and singles:
-        singles = _place_on_slots(singles, params)
+    if singles:
+        singles = _place_on_slots(singles, params, params.num_cus if balanced else NUM_XCDS)
 
     T = params.q_tile if params.q_tile > 0 else 256 // group
     chunks = []

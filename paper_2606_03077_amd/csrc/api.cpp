@@ -422,7 +422,7 @@ libra_status libra_xcd_read_weights(const void* buf, size_t bytes, int32_t reps,
   if (!buf || !weights) return set_error(LIBRA_E_INVAL, "buf or weights is NULL");
   if (reinterpret_cast<uintptr_t>(buf) % kWorkspaceAlign)
     return set_error(LIBRA_E_INVAL, "buf must be 256-byte aligned");
-  if (bytes < (size_t(64) << 20)) return set_error(LIBRA_E_INVAL, "buf must hold at least 64 MiB");
+  if (bytes < (size_t(1) << 30)) return set_error(LIBRA_E_INVAL, "buf must hold at least 1 GiB");
   if (reps < 1 || reps > 100) return set_error(LIBRA_E_INVAL, "reps must lie in [1, 100]");
   return measure_xcd_weights(buf, bytes, reps, weights, static_cast<hipStream_t>(stream));
 }

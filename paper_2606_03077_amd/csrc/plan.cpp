@@ -50,13 +50,14 @@ bool one_wave_splits(const std::vector<int64_t>& pages, const std::vector<int64_
   return true;
 }
 
-// Rule step 11: the units (in step 9's order) are dealt to compute-unit slots, each to
-// the slot with room that minimises (load + cost) / weight; the r-th unit of slot c is
-// listed at position c + r * num_cus.  Slots of one XCD share a weight, so one min-heap of
-// (load, c) per XCD yields that XCD's best slot and the eight candidates are compared
-// exactly; this picks the same slot as a scan over all of them.
-std::vector<Unit> place_on_slots(const std::vector<Unit>& units, const libra_plan_params& p) {
-  const int64_t n = int64_t(units.size()), S = p.num_cus;
+// Rule step 11: the units (in step 9's order) are dealt to S slots, each to the slot with
+// room that minimises (load + cost) / weight; the r-th unit of slot c is listed at position
+// c + r * S.  Slots of one XCD share a weight, so one min-heap of (load, c) per XCD yields
+// that XCD's best slot and the eight candidates are compared exactly; this picks the same
+// slot as a scan over all of them.
+std::vector<Unit> place_on_slots(const std::vector<Unit>& units, const libra_plan_params& p,
+                                 int64_t S) {
+  const int64_t n = int64_t(units.size());
   auto weight = [&](int64_t c) -> int64_t {
     const int32_t x = p.xcd_weight[c % kNumXcds];
     return x > 0 ? x : 1000;
@@ -172,7 +173,8 @@ libra_status build_plan(const libra_plan_desc& d, const int32_t* seq_lens, const
     if (x[U_G] != y[U_G]) return x[U_G] < y[U_G];
     return x[U_SPLIT] < y[U_SPLIT];
   });
-  if (balanced && !singles.empty()) singles = place_on_slots(singles, p);  // step 11
+  if (!singles.empty())  // step 11: CU slots for one wave, else the XCD queues
+    singles = place_on_slots(singles, p, balanced ? int64_t(p.num_cus) : int64_t(kNumXcds));
 
   // Step 7: query tiles of chunk rows.
   const int64_t T = p.q_tile > 0 ? p.q_tile : int64_t(kChunkRows) / G;

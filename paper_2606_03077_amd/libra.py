@@ -305,7 +305,7 @@ def libra_splitkv_plan(mode: int, batch: int, num_q_heads: int, num_kv_heads: in
 
 
 def libra_xcd_read_weights(buf, reps: int = 5, stream=None) -> list:
-    """Per-XCD HBM read weights measured by streaming the device buffer `buf` (>= 64 MiB)."""
+    """Per-XCD HBM read weights measured by streaming the device buffer `buf` (>= 1 GiB)."""
     w = (ctypes.c_int32 * 8)()
     nbytes = buf.numel() * buf.element_size()
     _check(load().libra_xcd_read_weights(_ptr(buf), nbytes, reps, w, _stream(stream)),

@@ -171,12 +171,12 @@ def test_xcd_read_weights_validation_codes():
     w = (ctypes.c_int32 * 8)()
     fake, mib = 1 << 30, 1 << 20
     call = lambda buf, nbytes, reps, out=w: lib.libra_xcd_read_weights(buf, nbytes, reps, out, None)
-    assert call(None, 64 * mib, 1) == 1                 # NULL buffer
-    assert call(fake, 64 * mib, 1, None) == 1           # NULL weights
-    assert call(fake + 16, 64 * mib, 1) == 1            # not 256-byte aligned
-    assert call(fake, 64 * mib - 1, 1) == 1             # smaller than 64 MiB
-    assert call(fake, 64 * mib, 0) == 1                 # reps < 1
-    assert call(fake, 64 * mib, 101) == 1               # reps > 100
+    assert call(None, 1024 * mib, 1) == 1                 # NULL buffer
+    assert call(fake, 1024 * mib, 1, None) == 1           # NULL weights
+    assert call(fake + 16, 1024 * mib, 1) == 1            # not 256-byte aligned
+    assert call(fake, 1024 * mib - 1, 1) == 1           # smaller than 1 GiB
+    assert call(fake, 1024 * mib, 0) == 1                 # reps < 1
+    assert call(fake, 1024 * mib, 101) == 1               # reps > 100
 
 
 def test_layout_validation_codes():

@@ -18,8 +18,8 @@ pytestmark = pytest.mark.gpu
 
 
 def test_xcd_read_weights_are_sane():
-    buf = torch.empty(256 << 20, dtype=torch.uint8, device="cuda")
-    H.say("[case] xcd read weights, 256 MiB")
+    buf = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    H.say("[case] xcd read weights, 1 GiB")
     w = libra.libra_xcd_read_weights(buf, reps=3)
     H.say(f"[xcd] weights {w}")
     assert len(w) == 8
@@ -37,8 +37,9 @@ def test_weighted_one_wave_decode_matches_oracle(weights):
     b = wl.custom_batch(lens, num_q_heads=8, num_kv_heads=2, seed=51)
     cache = H.DeviceCache(b)
     if weights == "measured":
-        buf = torch.empty(64 << 20, dtype=torch.uint8, device="cuda")
+        buf = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
         weights = libra.libra_xcd_read_weights(buf, reps=1)
+        del buf
     params = dict(num_cus=16, units_per_cu=3, min_split_pages=2)
     if weights is not None:
         params["xcd_weight"] = list(weights)

@@ -13,6 +13,7 @@ def test_hand_derived_decode_example():
     # L = [40, 0, 100] -> pages [3, 0, 7]; W = 10, target = 1 * 2 = 2,
     # chunk = max(2, ceil(10 / 2)) = 5; n = [1, 1, 2].  Sequence 2 splits into pages
     # [0, 3) and [3, 7), i.e. tokens [0, 48) and [48, 100); its two slots start at 0.
+    # Step 11 deals the four units to XCD queues 0-3 in step 9's order (one each).
     units, info = plan_ref([40, 0, 100], None, 1, 4,
                            PlanParams(num_cus=1, units_per_cu=2, min_split_pages=2, max_splits=8))
     assert units == [
@@ -79,14 +80,14 @@ def test_few_groups_fill_every_queue():
     assert max(qcost) - min(qcost) <= 0.02 * sum(cost)
 
 
-def check_slot_placement(singles, params):
+def check_slot_placement(singles, params, S):
     """Step 11 read off the output: position w belongs to slot w % num_cus; slot c holds
     exactly the positions w < n with w % num_cus = c; replaying the units in step 9's
     order (descending KV tokens, ties (b, g, j)), each unit's slot had room and no slot
     with room had a smaller (load + cost) / weight, nor an equal one with a smaller
     index; and a slot's units keep step 9's order across its positions."""
     from fractions import Fraction
-    n, S = len(singles), params.num_cus
+    n = len(singles)
     w8 = [x if x > 0 else 1000 for x in params.xcd_weight]
     slot_of = {}
     for w, u in enumerate(singles):
@@ -130,6 +131,27 @@ def test_hand_derived_slot_placement():
     assert units == [unit(b) for b in (0, 1, 2, 4, 3, 5)]
 
 
+def test_hand_derived_xcd_queue_placement():
+    # Ten rows of 10, 9, ..., 1 pages, Hkv = 1, one CU x 2 units: more rows than R = 2, so
+    # the chunk rule keeps one split each (chunk = ceil(55 / 2) = 28 pages) and step 11
+    # deals the ten units to the 8 XCD queues: queues 0 and 1 take positions {0, 8} and
+    # {1, 9}, queues 2-7 one position each.  Equal weights: 10, 9, ..., 3 go to queues
+    # 0..7 in turn; 2 -> queue 1 (9 + 2 < 10 + 2); 1 -> queue 0, the only one with room.
+    pages = list(range(10, 0, -1))
+    lens = [16 * p for p in pages]
+    unit = lambda b: (b, 0, 0, lens[b], 0, 1, 0, 1, -1, b, 0, lens[b] - 1)
+    par = dict(num_cus=1, units_per_cu=2, min_split_pages=1)
+    units, info = plan_ref(lens, None, 1, 4, PlanParams(**par))
+    assert not info["balanced"]
+    assert units == [unit(b) for b in (0, 1, 2, 3, 4, 5, 6, 7, 9, 8)]
+    # Odd XCDs at half weight: 10, 9, 8, 7 -> even queues 0, 2, 4, 6 (x / 1000 < x / 500);
+    # 6 -> queue 1 (6 / 500 = 0.012 < 16 / 1000); 5, 4, 3 -> queues 3, 5, 7 (below 15, 14,
+    # 13 / 1000 on queue 0); 2 -> queue 0 (12 / 1000 < 8 / 500); 1 -> queue 1, the last room.
+    units, _ = plan_ref(lens, None, 1, 4,
+                        PlanParams(**par, xcd_weight=(1000, 500) * 4))
+    assert units == [unit(b) for b in (0, 4, 1, 5, 2, 6, 3, 7, 8, 9)]
+
+
 def test_slot_placement_catches_a_planted_mistake(monkeypatch):
     # A placement that ignores the weights breaks the replay check.
     import oracle.plan as op
@@ -138,10 +160,10 @@ def test_slot_placement_catches_a_planted_mistake(monkeypatch):
                         xcd_weight=(1000, 500, 0, 0, 0, 0, 0, 0))
     real = op._place_on_slots
     monkeypatch.setattr(op, "_place_on_slots",
-                        lambda units, p: real(units, dataclasses.replace(p, xcd_weight=(0,) * 8)))
+                        lambda units, p, S: real(units, dataclasses.replace(p, xcd_weight=(0,) * 8), S))
     units, _ = op.plan_ref(lens, None, 1, 4, params)
     with pytest.raises(AssertionError):
-        check_slot_placement(units, params)
+        check_slot_placement(units, params, 2)
 
 
 def check_invariants(seq_lens, q_lens, hkv, group, params):
@@ -151,12 +173,14 @@ def check_invariants(seq_lens, q_lens, hkv, group, params):
     singles = units[:info["n_single"]]
     chunks = units[info["n_single"]:]
     assert all(u[F["kind"]] == 0 for u in singles) and all(u[F["kind"]] == 1 for u in chunks)
-    # ordering: step 9's descending KV order, or in a one-wave plan step 11's slots
-    kv = [u[3] - u[2] for u in singles]
-    if info["balanced"] and singles:
-        check_slot_placement(singles, params)
-    else:
-        assert kv == sorted(kv, reverse=True)
+    # ordering: step 11's slots (CUs for a one-wave plan, else XCD queues), each slot's
+    # units in step 9's descending KV order
+    if singles:
+        S = params.num_cus if info["balanced"] else 8
+        check_slot_placement(singles, params, S)
+        for c in range(S):
+            kv = [u[3] - u[2] for u in singles[c::S]]
+            assert kv == sorted(kv, reverse=True)
     # chunk units: per-XCD queues, each (b, g) group contiguous inside one queue with its
     # tiles by descending cost, groups dealt to the least-loaded queue
     cost = lambda u: (u[3] - u[2]) * (u[5] - u[4])
