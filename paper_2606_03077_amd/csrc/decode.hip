@@ -15,9 +15,9 @@
 // in base 2 with the scale folded in; column maxima use two cross-lane shuffles.
 // The 4 waves' (max, sum, accumulator) are merged through LDS.  A unit that covers the
 // whole row writes bf16 O and the float32 LSE; a split writes a float32 partial, and
-// merge_kernel, launched next on the same stream, combines the partials of each split
-// row by their log-sum-exps (the launch boundary orders the two without device-wide
-// cache flushes inside either kernel).
+// merge_kernel (merge.hip), launched next on the same stream, combines the partials of
+// each split row by their log-sum-exps (the launch boundary orders the two without
+// device-wide cache flushes inside either kernel).
 #include <cmath>
 
 #include "internal.h"
@@ -309,78 +309,6 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(LIBRA_
   }
 }
 
-struct MergeArgs {
-  const int32_t* merges;
-  const float* part_o;
-  const float* part_lse;
-  uint16_t* out;
-  float* lse;
-  int hq;
-  int group;
-};
-
-// One 256-thread block per split (sequence, KV head): thread t finishes channels
-// 8 * (t % 16) .. + 7 of query head t / 16 of the group.  With M = max_j lse_j (base 2):
-// lse = M + log2(sum_j 2^(lse_j - M)), o = sum_j 2^(lse_j - lse) o_j; empty splits
-// (lse_j = -inf) add nothing.  Splits are read 8 at a time (all loads of a batch in
-// flight together) and folded in with a running maximum.
-__global__ __launch_bounds__(256) void merge_kernel(MergeArgs A) {
-  constexpr int kBatch = 8;
-  const int32_t* m = A.merges + size_t(blockIdx.x) * kMergeInts;
-  const int g = m[M_G], n = m[M_N], part = m[M_PART], row = m[M_ROW];
-  const int G = A.group;
-  const int tid = threadIdx.x;
-  const int hcol = tid >> 4, c8 = (tid & 15) * 8;
-  if (hcol >= G) return;
-  float M = -INFINITY, wsum = 0.f;
-  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  for (int j0 = 0; j0 < n; j0 += kBatch) {
-    float lj[kBatch];
-    f32x4 x0[kBatch], x1[kBatch];
-#pragma unroll
-    for (int jj = 0; jj < kBatch; ++jj) {
-      lj[jj] = -INFINITY;
-      x0[jj] = x1[jj] = f32x4{0.f, 0.f, 0.f, 0.f};
-      if (j0 + jj < n) {
-        const size_t slot = size_t(part + j0 + jj) * G + hcol;
-        lj[jj] = A.part_lse[slot];
-        const float* po = A.part_o + slot * kDim + c8;
-        x0[jj] = *reinterpret_cast<const f32x4*>(po);
-        x1[jj] = *reinterpret_cast<const f32x4*>(po + 4);
-      }
-    }
-    float Mc = M;
-#pragma unroll
-    for (int jj = 0; jj < kBatch; ++jj) Mc = fmaxf(Mc, lj[jj]);
-    if (Mc == -INFINITY) continue;
-    const float r = __builtin_amdgcn_exp2f(M - Mc);  // 0 while M = -inf
-    wsum *= r;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) acc[i] *= r;
-#pragma unroll
-    for (int jj = 0; jj < kBatch; ++jj) {
-      const float w = __builtin_amdgcn_exp2f(lj[jj] - Mc);  // 0 for empty or absent splits
-      wsum += w;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        acc[i] += w * x0[jj][i];
-        acc[4 + i] += w * x1[jj][i];
-      }
-    }
-    M = Mc;
-  }
-  const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
-  uint4 ov;
-  ov.x = pack_bf16x2(acc[0] * inv, acc[1] * inv);
-  ov.y = pack_bf16x2(acc[2] * inv, acc[3] * inv);
-  ov.z = pack_bf16x2(acc[4] * inv, acc[5] * inv);
-  ov.w = pack_bf16x2(acc[6] * inv, acc[7] * inv);
-  const size_t head = size_t(g) * G + hcol;
-  *reinterpret_cast<uint4*>(A.out + (size_t(row) * A.hq + head) * kDim + c8) = ov;
-  if (A.lse && (tid & 15) == 0)
-    A.lse[size_t(row) * A.hq + head] = wsum > 0.f ? (M + log2f(wsum)) * kLn2 : -INFINITY;
-}
-
 }  // namespace
 
 hipError_t launch_decode(const KvLayout& L, const Plan& P, void* ws, const void* q,
@@ -405,28 +333,6 @@ hipError_t launch_decode(const KvLayout& L, const Plan& P, void* ws, const void*
   A.group = P.group;
   A.sl2 = scale * kLog2e;
   hipLaunchKernelGGL(decode_kernel, dim3(unsigned(n)), dim3(kThreads), 0, s, A);
-  return hipGetLastError();
-}
-
-}  // namespace libra
-
-namespace libra {
-
-bool merge_launches(const Plan& P) { return P.info.n_merge_groups > 0; }
-
-hipError_t launch_merge(const Plan& P, void* ws, void* out, float* lse, hipStream_t s) {
-  const int n = P.info.n_merge_groups;
-  if (!merge_launches(P)) return hipSuccess;
-  char* w = static_cast<char*>(ws);
-  MergeArgs A;
-  A.merges = reinterpret_cast<const int32_t*>(w + P.off_merges);
-  A.part_o = reinterpret_cast<const float*>(w + P.off_part_o);
-  A.part_lse = reinterpret_cast<const float*>(w + P.off_part_lse);
-  A.out = static_cast<uint16_t*>(out);
-  A.lse = lse;
-  A.hq = P.num_q_heads;
-  A.group = P.group;
-  hipLaunchKernelGGL(merge_kernel, dim3(unsigned(n)), dim3(256), 0, s, A);
   return hipGetLastError();
 }
 
