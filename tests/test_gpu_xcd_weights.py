@@ -56,3 +56,31 @@ def test_weighted_one_wave_decode_matches_oracle(weights):
     ro, rl = oracle.decode_ref(b.q, b.k_pages, b.v_pages, b.block_table, b.seq_lens, b.scale)
     H.assert_parity(o, lse, ro, rl, label=f"weights {weights}")
     cache.close()
+
+
+@pytest.mark.parametrize("weights", [(1000, 850, 1000, 850, 1000, 850, 1000, 850),
+                                     (1, 1000000, 3, 999, 0, 500, 1000, 2)])
+def test_weighted_xcd_queue_decode_matches_oracle(weights):
+    # 40 rows on 4 CUs x 3 units, Hkv = 2: more rows than a wave, so the chunk rule cuts
+    # them (the 20,000-token row into pieces) and step 11 deals the units to the 8 XCD
+    # queues.
+    rng = np.random.default_rng(52)
+    lens = rng.integers(1, 3000, size=40).tolist()
+    lens[7] = 20000  # one row long enough for the chunk rule to split
+    H.say(f"[case] weighted XCD-queue decode weights={weights}")
+    b = wl.custom_batch(lens, num_q_heads=8, num_kv_heads=2, seed=53)
+    cache = H.DeviceCache(b)
+    params = dict(num_cus=4, units_per_cu=3, min_split_pages=4, xcd_weight=list(weights))
+    plan = H.plan_for(b, **params)
+    info = libra.libra_plan_get_info(plan)
+    assert info["balanced"] == 0 and info["n_merge_groups"] > 0
+    ref_units, _ = oracle.plan_ref(lens, None, 2, 4,
+                                   oracle.PlanParams(num_cus=4, units_per_cu=3, min_split_pages=4,
+                                                     xcd_weight=tuple(weights)))
+    assert np.array_equal(libra.libra_plan_get_units(plan),
+                          np.array(ref_units, np.int32).reshape(-1, 12))
+    libra.libra_plan_destroy(plan)
+    o, lse, _, _ = H.run(b, cache, plan_params=params)
+    ro, rl = oracle.decode_ref(b.q, b.k_pages, b.v_pages, b.block_table, b.seq_lens, b.scale)
+    H.assert_parity(o, lse, ro, rl, label=f"xcd queues, weights {weights}")
+    cache.close()
