@@ -7,7 +7,9 @@ merge of split rows) over the whole synthetic batch, inputs resident in HBM.  Be
 timed step an untimed 1 GiB fill evicts L2 and the 256 MB MALL, so every step reads its
 KV from HBM.  Each step is bracketed by HIP events on the stream the kernel runs on.
 The host-side split plan is built once per batch step and shared by all layers of a
-model; its time is reported separately (``plan_ms``) and is not part of a step.
+model; its time is reported separately (``plan_ms``) and is not part of a step.  Before
+planning, the per-XCD HBM read weights that the plan's slot placement takes are measured
+once on the flush buffer (``libra_xcd_read_weights``; ``--xcd-weights equal`` skips it).
 
 Prints one JSON line (rank 0, N = 1):
   value = algorithmic KV bytes / mean step time (TB/s), plus decode tokens/s, the

@@ -262,3 +262,41 @@ def test_workspace_size_accounts_for_partials():
     need = info["n_units"] * 48 + 4 * 8 * 4 + info["n_partial_slots"] * G * 129 * 4
     assert ws >= need and ws % 256 == 0
     libra.libra_plan_destroy(plan)
+
+
+def test_traffic_keys_follow_the_unit_set():
+    """bench.py keys committed HBM counters to a hash of the plan's set of units: the same
+    units in any order (e.g. placed with other XCD weights) share the key, another set does
+    not, and every committed entry's key is the current plan's for its workload."""
+    import json
+    import os
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    sys.path.insert(0, root)
+    import bench
+    w = wl.WORKLOADS["7b"]
+    lens, _ = wl.draw_lengths(w, np.random.default_rng(w.seed))
+    keys = set()
+    for weights in ([0] * 8, [1000, 850] * 4, [1, 1000000, 7, 900, 0, 3, 1000, 500]):
+        h = libra.libra_splitkv_plan(libra.LIBRA_MODE_DECODE, len(lens), w.num_q_heads,
+                                     w.num_kv_heads, lens.tolist(), None, num_cus=256,
+                                     xcd_weight=weights)
+        units = libra.libra_plan_get_units(h)
+        libra.libra_plan_destroy(h)
+        keys.add(bench.plan_sha(units))
+        shuffled = units[np.random.default_rng(5).permutation(len(units))]
+        assert bench.plan_sha(shuffled) == bench.plan_sha(units)
+        assert bench.plan_sha(units[1:]) != bench.plan_sha(units)
+    assert len(keys) == 1
+    with open(os.path.join(root, "profiles", "counters.json")) as f:
+        counters = json.load(f)
+    for kernel in ("decode_kernel", "chunk_kernel"):
+        for name, entry in counters.get(kernel, {}).items():
+            wk = wl.WORKLOADS[name]
+            lens, qlens = wl.draw_lengths(wk, np.random.default_rng(wk.seed))
+            mode = libra.LIBRA_MODE_APPEND if wk.append else libra.LIBRA_MODE_DECODE
+            h = libra.libra_splitkv_plan(mode, len(lens), wk.num_q_heads, wk.num_kv_heads,
+                                         lens.tolist(), qlens.tolist() if wk.append else None,
+                                         num_cus=256)
+            assert entry["plan_sha"] == bench.plan_sha(libra.libra_plan_get_units(h)), (kernel, name)
+            libra.libra_plan_destroy(h)
