@@ -33,6 +33,9 @@ def _case(seed):
                   min_split_pages=int(rng.choice([1, 2, 4, 16])),
                   max_splits=int(rng.choice([1, 2, 8, 64])),
                   q_tile=int(rng.choice([0, 1, 16, 256 // g])))
+    # drawn last so the earlier draws (and cases) stay as they were
+    weights = [int(x) for x in rng.choice([0, 1, 500, 910, 1000, 1000000], size=8)]
+    params["xcd_weight"] = weights if seed % 3 else [0] * 8
     return g * hkv, hkv, lens, q_lens, params
 
 
