@@ -286,6 +286,8 @@ def libra_splitkv_plan(mode: int, batch: int, num_q_heads: int, num_kv_heads: in
                        num_cus: int = 0, units_per_cu: int = 3, min_split_pages: int = 16,
                        max_splits: int = 64, q_tile: int = 0,
                        xcd_weight: Optional[Sequence[int]] = None) -> int:
+    """Builds a split plan (rule in include/libra.h).  xcd_weight: 8 relative HBM read rates
+    of the XCDs for the slot placement (e.g. from libra_xcd_read_weights); None = equal."""
     d = PlanDesc(mode, batch, num_q_heads, num_kv_heads)
     w = list(xcd_weight) if xcd_weight is not None else [0] * 8
     if len(w) != 8:
