@@ -14,6 +14,7 @@ import math
 import numpy as np
 import pytest
 
+import oracle.cost_model as ocm
 from oracle.cost_model import (ce_fit_ref, instance_cost, mape_ref, partition_makespan,
                                poly_eval, poly_sum_ref, rollout_dp_ref, sorted_order)
 
@@ -70,6 +71,44 @@ def test_trajectory_sum_textbook(a, b):
 MODEL = {"attn_step": (2e-9, 1e-6, 0.0),
          "linear_step": [1.0e-3, 0.6e-3, 0.36e-3, 0.25e-3],
          "attn_scale": [1.0, 0.52, 0.27, 0.15]}
+
+
+# Hand-sized model for the by-hand pins below: T_attn_step(l) = l + 2, per-step
+# non-attention time 10 at TP 1 and 6 at TP 2, attention scaled by 1 at TP 1 and 0.5 at TP 2.
+HAND = {"attn_step": (0.0, 1.0, 2.0), "linear_step": [10.0, 6.0, 0.0, 0.0],
+        "attn_scale": [1.0, 0.5, 0.0, 0.0]}
+
+
+def test_instance_cost_by_hand():
+    """Cost(tp, a, b) of Alg. 1 under the library's reading (an instance batches all its
+    requests: as many decode steps as its longest request, each paying the TP's
+    per-step time, plus every request's trajectory attention sum_{l=1..len} T(l),
+    scaled per TP), worked out by hand for requests of 2, 3 and 5 tokens:
+
+      trajectory attention: len 2 -> (1+2) + (2+2) = 7
+                            len 3 -> 3 + 4 + 5     = 12
+                            len 5 -> 3+4+5+6+7     = 25      total 44
+      TP 1: 10 * max(2, 3, 5) + 1.0 * 44 = 50 + 44 = 94
+      TP 2:  6 * 5            + 0.5 * 44 = 30 + 22 = 52
+      one request of 5 at TP 1: 10 * 5 + 25 = 75; of 2 and 3: 10 * 3 + 19 = 49
+    """
+    assert ocm.instance_cost(HAND, 1, [2, 3, 5]) == 94.0
+    assert ocm.instance_cost(HAND, 2, [2, 3, 5]) == 52.0
+    assert ocm.instance_cost(HAND, 1, [5]) == 75.0
+    assert ocm.instance_cost(HAND, 1, [2, 3]) == 49.0
+    assert ocm.instance_cost(HAND, 2, []) == 0.0
+
+
+def test_rollout_dp_by_hand():
+    """Two GPUs, degrees {1, 2}, requests 5, 2, 3 (sorted: 2, 3, 5), by hand from the costs
+    of test_instance_cost_by_hand: one TP-2 instance costs 52; two TP-1 instances with
+    contiguous runs cost max(0, 94) = 94, max(27, 87) = 87 (runs [2] and [3, 5]:
+    10 * 2 + 7 = 27, 10 * 5 + 12 + 25 = 87) or max(49, 75) = 75.  Best: 52, TP 2."""
+    ms, order, inst = ocm.rollout_dp_ref([5, 2, 3], 2, [1, 2], HAND)
+    assert ms == 52.0
+    assert order == [1, 2, 0] and inst == [(2, 0, 3)]
+    ms1, _, inst1 = ocm.rollout_dp_ref([5, 2, 3], 2, [1], HAND)
+    assert ms1 == 75.0 and sorted(inst1) == [(1, 0, 2), (1, 2, 1)]
 
 
 def compositions(n, parts):

@@ -87,6 +87,31 @@ def test_causal_off_by_one_is_caught(monkeypatch):
     assert _caught(pins.test_append_matches_torch_sdpa_lower_right_causal, 7, 9)
 
 
+def _bf16_shift_by_15(bits):
+    b = np.asarray(bits, dtype=np.uint16).astype(np.uint32) << np.uint32(15)
+    return b.view(np.float32).astype(np.float64)
+
+
+def _bf16_sign_dropped(bits):
+    b = (np.asarray(bits, dtype=np.uint16) & np.uint16(0x7FFF)).astype(np.uint32) << np.uint32(16)
+    return b.view(np.float32).astype(np.float64)
+
+
+def _bf16_fraction_truncated(bits):
+    b = (np.asarray(bits, dtype=np.uint16) & np.uint16(0xFFFE)).astype(np.uint32) << np.uint32(16)
+    return b.view(np.float32).astype(np.float64)
+
+
+@pytest.mark.parametrize("mutant", [_bf16_shift_by_15, _bf16_sign_dropped,
+                                    _bf16_fraction_truncated], ids=lambda f: f.__name__)
+def test_bf16_decoder_mutants_are_caught(monkeypatch, mutant):
+    """A wrong bf16 decoder fails the exhaustive decoder pin, and, since the SDPA
+    references decode their inputs with torch's own bfloat16, the attention pin too."""
+    monkeypatch.setattr(oa, "bf16_bits_to_f64", mutant)
+    assert _caught(pins.test_bf16_decoder_matches_torch_on_every_bit_pattern)
+    assert _caught(pins.test_decode_matches_torch_sdpa, 8, 2)
+
+
 def test_merge_sign_slip_is_caught(monkeypatch):
     real = oa.merge_ref
 
@@ -138,6 +163,45 @@ def test_unweighted_fit_is_caught(monkeypatch):
 
     monkeypatch.setattr(cm, "ce_fit_ref", absolute_fit)
     assert _caught(cm.test_fit_normal_equations_hold)
+
+
+def _cost_sum_not_max(model, tp, seg_lengths):
+    if len(seg_lengths) == 0:
+        return 0.0
+    import oracle.cost_model as ocm
+    s = ocm.TP_SLOTS[tp]
+    attn = sum(ocm.trajectory_attention(tuple(model["attn_step"]), int(x)) for x in seg_lengths)
+    return model["linear_step"][s] * sum(seg_lengths) + model["attn_scale"][s] * attn
+
+
+def _cost_attention_unscaled(model, tp, seg_lengths):
+    if len(seg_lengths) == 0:
+        return 0.0
+    import oracle.cost_model as ocm
+    s = ocm.TP_SLOTS[tp]
+    attn = sum(ocm.trajectory_attention(tuple(model["attn_step"]), int(x)) for x in seg_lengths)
+    return model["linear_step"][s] * max(seg_lengths) + attn
+
+
+def _cost_attention_of_longest_only(model, tp, seg_lengths):
+    if len(seg_lengths) == 0:
+        return 0.0
+    import oracle.cost_model as ocm
+    s = ocm.TP_SLOTS[tp]
+    attn = ocm.trajectory_attention(tuple(model["attn_step"]), int(max(seg_lengths)))
+    return model["linear_step"][s] * max(seg_lengths) + model["attn_scale"][s] * attn
+
+
+@pytest.mark.parametrize("mutant", [_cost_sum_not_max, _cost_attention_unscaled,
+                                    _cost_attention_of_longest_only], ids=lambda f: f.__name__)
+def test_instance_cost_mutants_are_caught(monkeypatch, mutant):
+    """Plausible misreadings of Cost(tp, a, b) fail the hand-computed pins (the brute
+    force and the DP both call instance_cost, so they cannot catch these)."""
+    import oracle.cost_model as ocm
+    import test_cost_model_oracle as cm
+    monkeypatch.setattr(ocm, "instance_cost", mutant)
+    assert _caught(cm.test_instance_cost_by_hand)
+    assert _caught(cm.test_rollout_dp_by_hand)
 
 
 def test_dp_segment_off_by_one_is_caught(monkeypatch):

@@ -16,10 +16,41 @@ import torch.nn.functional as F
 from torch.nn.attention.bias import causal_lower_right
 
 import oracle
-from oracle.attention import attend, bf16_bits_to_f64, gather_tokens
+import oracle.attention as oa
+from oracle.attention import attend, gather_tokens
 from paper_2606_03077_amd import workloads as wl
 
 D = 128
+
+
+def _torch_bf16(bits) -> np.ndarray:
+    """bf16 bit patterns decoded by torch's own bfloat16 type, widened to float64.
+
+    The SDPA references below take their inputs through this decoder, not the oracle's,
+    so a slip in the oracle's bf16 decoding shows up as a disagreement."""
+    a = np.ascontiguousarray(np.asarray(bits, dtype=np.uint16)).view(np.int16)
+    return torch.from_numpy(a).view(torch.bfloat16).double().numpy()
+
+
+def test_bf16_decoder_matches_torch_on_every_bit_pattern():
+    """All 65,536 bf16 patterns decode to torch's bfloat16 values (NaN where torch gives
+    NaN), plus closed forms read off the format: sign bit 15, 8 exponent bits with bias
+    127, 7 fraction bits, subnormals below exponent 1."""
+    bits = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    got = oa.bf16_bits_to_f64(bits)
+    ref = _torch_bf16(bits)
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(got), nan)
+    assert np.array_equal(got[~nan], ref[~nan])
+    assert np.array_equal(np.signbit(got[~nan]), np.signbit(ref[~nan]))   # -0.0 included
+    closed = {0x0000: 0.0, 0x3F80: 1.0, 0xBF80: -1.0, 0x4000: 2.0, 0xC040: -3.0,
+              0x3F81: 1.0 + 2.0 ** -7, 0x3E00: 0.125, 0x7F7F: (2.0 - 2.0 ** -7) * 2.0 ** 127,
+              0x0080: 2.0 ** -126, 0x0001: 2.0 ** -133, 0x807F: -(127 * 2.0 ** -133),
+              0x7F80: math.inf, 0xFF80: -math.inf}
+    for b, v in closed.items():
+        assert oa.bf16_bits_to_f64(np.array([b], np.uint16))[0] == v, hex(b)
+    assert np.signbit(oa.bf16_bits_to_f64(np.array([0x8000], np.uint16))[0])
+    assert np.isnan(oa.bf16_bits_to_f64(np.array([0x7FC0, 0xFFC1, 0x7F81], np.uint16))).all()
 
 
 def _scatter_contiguous(K, block_table_row, pages, g):
@@ -78,9 +109,9 @@ def test_decode_matches_torch_sdpa(Hq, Hkv):
     G = Hq // Hkv
     for b, L in enumerate(lens):
         # KV heads repeated G times in contiguous groups (torch repeat_interleave)
-        K = np.repeat(bf16_bits_to_f64(Ks[b]), G, axis=0)
-        V = np.repeat(bf16_bits_to_f64(Vs[b]), G, axis=0)
-        qq = bf16_bits_to_f64(q[b])[:, None, :]
+        K = np.repeat(_torch_bf16(Ks[b]), G, axis=0)
+        V = np.repeat(_torch_bf16(Vs[b]), G, axis=0)
+        qq = _torch_bf16(q[b])[:, None, :]
         ro, rl = _sdpa(qq, K, V, scale)
         np.testing.assert_allclose(o[b], ro[:, 0], rtol=0, atol=1e-12)
         np.testing.assert_allclose(lse[b], rl[:, 0], rtol=0, atol=1e-12)
@@ -102,9 +133,9 @@ def test_append_matches_torch_sdpa_lower_right_causal(prior, chunk):
     scale = 0.0883883461356163
     o, lse, kp2, vp2 = oracle.append_ref(q, k_new, v_new, kp, vp, bt, np.array([L]),
                                          np.array([chunk]), scale)
-    K = np.repeat(bf16_bits_to_f64(Ks[0]), G, axis=0)
-    V = np.repeat(bf16_bits_to_f64(Vs[0]), G, axis=0)
-    qq = bf16_bits_to_f64(q).transpose(1, 0, 2)  # [Hq, chunk, d]
+    K = np.repeat(_torch_bf16(Ks[0]), G, axis=0)
+    V = np.repeat(_torch_bf16(Vs[0]), G, axis=0)
+    qq = _torch_bf16(q).transpose(1, 0, 2)  # [Hq, chunk, d]
     mask = causal_lower_right(chunk, L)._materialize("cpu")
     ro, rl = _sdpa(qq, K, V, scale, mask)
     np.testing.assert_allclose(o.transpose(1, 0, 2), ro, rtol=0, atol=1e-12)
@@ -123,8 +154,8 @@ def test_single_key_returns_v_exactly():
     for b in range(2):
         for h in range(8):
             g = h // 4
-            assert np.array_equal(o[b, h], bf16_bits_to_f64(Vs[b][g, 0]))
-            ref = scale * float(np.dot(bf16_bits_to_f64(q[b, h]), bf16_bits_to_f64(Ks[b][g, 0])))
+            assert np.array_equal(o[b, h], _torch_bf16(Vs[b][g, 0]))
+            ref = scale * float(np.dot(_torch_bf16(q[b, h]), _torch_bf16(Ks[b][g, 0])))
             assert abs(lse[b, h] - ref) <= 1e-12 * max(1.0, abs(ref))
 
 
@@ -136,10 +167,10 @@ def test_identical_keys_give_mean_v_and_log_n():
     for t in range(L):
         kp[bt[0, t // 16], 0, t % 16] = k0
     o, lse = oracle.decode_ref(q, kp, vp, bt, np.array([L]), 0.1)
-    mean_v = bf16_bits_to_f64(Vs[0][0]).mean(axis=0)
+    mean_v = _torch_bf16(Vs[0][0]).mean(axis=0)
     for h in range(4):
         np.testing.assert_allclose(o[0, h], mean_v, rtol=0, atol=1e-13)
-        ref = 0.1 * np.dot(bf16_bits_to_f64(q[0, h]), bf16_bits_to_f64(k0)) + math.log(L)
+        ref = 0.1 * np.dot(_torch_bf16(q[0, h]), _torch_bf16(k0)) + math.log(L)
         assert abs(lse[0, h] - ref) < 1e-12
 
 
@@ -150,7 +181,7 @@ def test_zero_query_gives_mean_v_and_log_n():
     q[:] = 0
     o, lse = oracle.decode_ref(q, kp, vp, bt, np.array([L]), 0.088)
     for h in range(2):
-        np.testing.assert_allclose(o[0, h], bf16_bits_to_f64(Vs[0][h]).mean(axis=0), atol=1e-13, rtol=0)
+        np.testing.assert_allclose(o[0, h], _torch_bf16(Vs[0][h]).mean(axis=0), atol=1e-13, rtol=0)
         assert abs(lse[0, h] - math.log(L)) < 1e-13
 
 
@@ -161,7 +192,7 @@ def test_dominant_key_selects_its_value():
     q[0, 0] = wl.f32_to_bf16_bits(np.full(D, 1.0, np.float32))
     kp[bt[0, 0], 0, 7] = wl.f32_to_bf16_bits(np.full(D, 4.0, np.float32))  # logit 512 above the rest
     o, lse = oracle.decode_ref(q, kp, vp, bt, np.array([L]), 1.0)
-    np.testing.assert_allclose(o[0, 0], bf16_bits_to_f64(Vs[0][0, 7]), atol=1e-12, rtol=0)
+    np.testing.assert_allclose(o[0, 0], _torch_bf16(Vs[0][0, 7]), atol=1e-12, rtol=0)
 
 
 def test_lse_matches_scipy_logsumexp():
@@ -290,10 +321,10 @@ def test_generator_is_deterministic_and_poisoned():
     for s in range(a.workload.batch):
         L = int(a.seq_lens[s])
         toks = gather_tokens(a.k_pages, a.block_table[s], 0, L)
-        assert not np.isnan(bf16_bits_to_f64(toks)).any()
+        assert not np.isnan(_torch_bf16(toks)).any()
         if L % 16:
             last = a.k_pages[a.block_table[s, (L - 1) // 16], 0, L % 16:]
-            assert np.isnan(bf16_bits_to_f64(last)).all()
+            assert np.isnan(_torch_bf16(last)).all()
     lens = wl.draw_lengths(wl.WORKLOADS["longtail"], np.random.default_rng(26063))[0]
     assert (lens > 4096).sum() == 26 and lens.max() <= 65536 and lens.min() >= 512
 
