@@ -21,8 +21,11 @@
  *   uses it.  A handle is destroyed only after the calls that use it were issued.
  * - Work is enqueued asynchronously on `stream` (a hipStream_t; NULL = the null stream).
  *   No entry point synchronises the device or allocates device memory, except
- *   libra_plan_destroy, which waits for its own pending upload.  A plan's first upload
- *   allocates its pinned host copy of the tables (freed by libra_plan_destroy).
+ *   libra_xcd_read_weights (set-up) and libra_plan_destroy, which waits for the plan's
+ *   own pending table upload (an event, not the device).  libra_splitkv_plan takes the
+ *   plan's pinned host image of its tables and an upload event from a library-owned pool
+ *   (allocating them only when the pool has none free); libra_plan_destroy returns them
+ *   to the pool.  Decode, append and upload calls allocate nothing.
  * - Host-only entry points (plan construction, cost evaluator, RolloutDP, prefix tree,
  *   routing, libra_kv_reshard_host) touch no GPU; the reshard may use up to 8 host
  *   threads for large runs.
@@ -263,7 +266,12 @@ typedef struct libra_plan_info {
 
 /* Builds the plan from host lengths.  seq_lens_host: int32 [batch], L_b >= 0 (>= C_b
  * for append).  q_lens_host: int32 [batch], C_b >= 1, for append; NULL for decode.
- * params may be NULL (defaults).  Pure host code apart from num_cus = 0. */
+ * params may be NULL (defaults).  The tables are computed on the host (querying the
+ * device only for num_cus = 0).  When a HIP device is visible, the plan also takes a
+ * pinned host image of its tables and an upload event from the library's pool
+ * (LIBRA_E_HIP if that allocation fails); without one, the plan serves inspection
+ * (libra_plan_get_units / _info) and its decode / append / upload calls return
+ * LIBRA_E_INVAL. */
 libra_status libra_splitkv_plan(const libra_plan_desc* desc, const int32_t* seq_lens_host,
                                 const int32_t* q_lens_host, const libra_plan_params* params,
                                 libra_plan* out);
@@ -303,7 +311,10 @@ void libra_plan_destroy(libra_plan plan);
 /* ------------------------------------------------------------------------------ */
 /*
  * Decode: one query token per sequence attends all L_b cached tokens (the current
- * token's K/V is already in the cache).  For each query head h of sequence b:
+ * token's K/V is already in the cache).  This is the per-step operation of rollout,
+ * autoregressive decoding that the paper finds bound by memory bandwidth and KV-cache
+ * pressure (Sec. 1; Sec. 2.1; App. A.1), over a batch whose lengths are long-tailed
+ * (Sec. 2.2).  For each query head h of sequence b:
  *   z_j = scale * <q_h, k_j>,  out = sum_j softmax(z)_j v_j,  lse = log sum_j exp(z_j)
  * over keys j in [0, L_b); L_b = 0 gives out = 0, lse = -inf.
  *
@@ -311,7 +322,8 @@ void libra_plan_destroy(libra_plan plan);
  * [batch][num_q_heads] or NULL.  block_table: device int32 [batch][bt_stride] with at
  * least ceil(L_b / 16) valid page ids per row.  The plan must be a decode plan built for
  * the same (batch, num_q_heads, num_kv_heads) and lengths; workspace: device, at least
- * libra_plan_workspace_bytes(plan) bytes, 256-byte aligned.  `scale` must be finite.
+ * libra_plan_workspace_bytes(plan) bytes, 256-byte aligned.  `scale` must be finite and
+ * positive (LIBRA_E_INVAL otherwise).
  * Split rows write float32 partials; a second launch on the same stream merges them by
  * their log-sum-exps.
  *

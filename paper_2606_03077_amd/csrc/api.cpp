@@ -121,36 +121,85 @@ bool holds_tables(const void* ws, uint64_t id) {
   return it != g_ws.owner.end() && it->second == id;
 }
 
-// Copies the plan's tables into ws unless ws already holds them (or always, if forced).
-libra_status upload(Plan& P, void* ws, size_t ws_bytes, hipStream_t s, bool force = true) {
-  std::lock_guard<std::mutex> lk(P.upload_mu);
-  if (!force && holds_tables(ws, P.id)) return LIBRA_OK;
-  if (!ws) return set_error(LIBRA_E_INVAL, "workspace is NULL");
-  if (reinterpret_cast<uintptr_t>(ws) % kWorkspaceAlign)
-    return set_error(LIBRA_E_INVAL, "workspace must be 256-byte aligned");
-  if (ws_bytes < P.ws_bytes)
-    return set_error(LIBRA_E_WORKSPACE, "workspace smaller than libra_plan_workspace_bytes");
-  hipError_t e;
-  if (!P.pinned && P.upload_bytes > 0) {
-    e = hipHostMalloc(&P.pinned, P.upload_bytes, hipHostMallocDefault);
-    if (e != hipSuccess) {
-      P.pinned = nullptr;
-      return hip_error(e, "hipHostMalloc(plan tables)");
+// Pinned staging images and upload events, owned by the library and reused by plans.
+// A plan takes one of each when it is built (libra_splitkv_plan) and returns them when it
+// is destroyed, so decode / append calls never allocate, and destroying a plan frees no
+// pinned memory (hipHostFree may wait for the device).  The pool never shrinks: it holds
+// as many images as plans were alive at once, and is never destroyed (its memory is not
+// freed at exit, when the HIP runtime may already be torn down).
+struct StagingPool {
+  std::mutex mu;
+  std::vector<std::pair<size_t, void*>> images;  // (capacity, pinned host memory)
+  std::vector<hipEvent_t> events;
+};
+StagingPool& g_staging = *new StagingPool();
+
+libra_status staging_acquire(Plan& P) {
+  std::lock_guard<std::mutex> lk(g_staging.mu);
+  if (P.upload_bytes > 0) {
+    size_t best = g_staging.images.size();
+    for (size_t i = 0; i < g_staging.images.size(); ++i)
+      if (g_staging.images[i].first >= P.upload_bytes &&
+          (best == g_staging.images.size() ||
+           g_staging.images[i].first < g_staging.images[best].first))
+        best = i;
+    if (best < g_staging.images.size()) {
+      P.pinned_capacity = g_staging.images[best].first;
+      P.pinned = g_staging.images[best].second;
+      g_staging.images.erase(g_staging.images.begin() + static_cast<std::ptrdiff_t>(best));
+    } else {
+      size_t cap = 4096;
+      while (cap < P.upload_bytes) cap *= 2;
+      hipError_t e = hipHostMalloc(&P.pinned, cap, hipHostMallocDefault);
+      if (e != hipSuccess) {
+        P.pinned = nullptr;
+        return hip_error(e, "hipHostMalloc(plan tables)");
+      }
+      P.pinned_capacity = cap;
     }
-    std::memset(P.pinned, 0, P.upload_bytes);
-    char* h = static_cast<char*>(P.pinned);
-    std::memcpy(h + P.off_units, P.units.data(), P.units.size() * sizeof(int32_t));
-    std::memcpy(h + P.off_writes, P.writes.data(), P.writes.size() * sizeof(int32_t));
-    std::memcpy(h + P.off_merges, P.merges.data(), P.merges.size() * sizeof(int32_t));
-    std::memcpy(h + P.off_xcd_map, P.xcd_map.data(), P.xcd_map.size() * sizeof(int32_t));
   }
-  if (!P.upload_done) {
-    e = hipEventCreateWithFlags(&P.upload_done, hipEventDisableTiming);
+  if (!g_staging.events.empty()) {
+    P.upload_done = g_staging.events.back();
+    g_staging.events.pop_back();
+  } else {
+    hipError_t e = hipEventCreateWithFlags(&P.upload_done, hipEventDisableTiming);
     if (e != hipSuccess) {
       P.upload_done = nullptr;
-      return hip_error(e, "hipEventCreate");
+      return hip_error(e, "hipEventCreate(plan upload)");
     }
   }
+  return LIBRA_OK;
+}
+
+void staging_release(Plan& P) {
+  std::lock_guard<std::mutex> lk(g_staging.mu);
+  if (P.pinned) g_staging.images.emplace_back(P.pinned_capacity, P.pinned);
+  if (P.upload_done) g_staging.events.push_back(P.upload_done);
+  P.pinned = nullptr;
+  P.upload_done = nullptr;
+}
+
+// Fills the plan's pinned image with its tables (at plan creation).
+void staging_fill(Plan& P) {
+  if (!P.pinned) return;
+  char* h = static_cast<char*>(P.pinned);
+  std::memset(h, 0, P.upload_bytes);
+  auto put = [h](size_t off, const std::vector<int32_t>& v) {
+    if (!v.empty()) std::memcpy(h + off, v.data(), v.size() * sizeof(int32_t));
+  };
+  put(P.off_units, P.units);
+  put(P.off_writes, P.writes);
+  put(P.off_merges, P.merges);
+  put(P.off_xcd_map, P.xcd_map);
+}
+
+// Enqueues the copy of the plan's pinned table image to ws and records its event.
+// Allocates nothing.  Caller holds P.upload_mu.
+libra_status enqueue_tables(Plan& P, void* ws, hipStream_t s) {
+  if (!P.upload_done)
+    return set_error(LIBRA_E_INVAL,
+                     "plan was built without a visible HIP device; it cannot run on one");
+  hipError_t e;
   {
     ProfScope ps(LIBRA_KERNEL_UPLOAD, s, true);
     if (P.upload_bytes > 0) {
@@ -160,6 +209,20 @@ libra_status upload(Plan& P, void* ws, size_t ws_bytes, hipStream_t s, bool forc
   }
   e = hipEventRecord(P.upload_done, s);
   if (e != hipSuccess) return hip_error(e, "hipEventRecord");
+  return LIBRA_OK;
+}
+
+// Copies the plan's tables into ws unless ws already holds them (or always, if forced).
+libra_status upload(Plan& P, void* ws, size_t ws_bytes, hipStream_t s, bool force = true) {
+  std::lock_guard<std::mutex> lk(P.upload_mu);
+  if (!force && holds_tables(ws, P.id)) return LIBRA_OK;
+  if (!ws) return set_error(LIBRA_E_INVAL, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(ws) % kWorkspaceAlign)
+    return set_error(LIBRA_E_INVAL, "workspace must be 256-byte aligned");
+  if (ws_bytes < P.ws_bytes)
+    return set_error(LIBRA_E_WORKSPACE, "workspace smaller than libra_plan_workspace_bytes");
+  libra_status st = enqueue_tables(P, ws, s);
+  if (st != LIBRA_OK) return st;
   {
     std::lock_guard<std::mutex> lk2(g_ws.mu);
     g_ws.owner[reinterpret_cast<uintptr_t>(ws)] = P.id;
@@ -178,7 +241,8 @@ libra_status check_call(const KvLayout* L, const Plan* P, int mode, const void* 
     return set_error(LIBRA_E_INVAL, "batch / num_q_heads differ from the plan's");
   if (P->num_kv_heads != L->desc.num_kv_heads)
     return set_error(LIBRA_E_INVAL, "plan and layout disagree on num_kv_heads");
-  if (!std::isfinite(scale)) return set_error(LIBRA_E_INVAL, "scale must be finite");
+  if (!(scale > 0.f) || !std::isfinite(scale))
+    return set_error(LIBRA_E_INVAL, "scale must be positive and finite");
   if (P->info.n_rows > 0) {
     if (!q || !out) return set_error(LIBRA_E_INVAL, "q / out is NULL");
     if (!aligned16(q) || !aligned16(out)) return set_error(LIBRA_E_INVAL, "q / out must be 16-byte aligned");
@@ -413,6 +477,20 @@ libra_status libra_splitkv_plan(const libra_plan_desc* desc, const int32_t* seq_
     delete P;
     return st;
   }
+  // Pinned staging for the table upload, taken here so that no decode / append call
+  // allocates.  Without a visible device (host-only use: inspecting a plan) there is none.
+  int n_dev = 0;
+  if (hipGetDeviceCount(&n_dev) != hipSuccess || n_dev <= 0) {
+    (void)hipGetLastError();
+  } else {
+    st = staging_acquire(*P);
+    if (st != LIBRA_OK) {
+      staging_release(*P);
+      delete P;
+      return st;
+    }
+    staging_fill(*P);
+  }
   *out = P;
   return LIBRA_OK;
 }
@@ -449,16 +527,15 @@ libra_status libra_plan_upload(libra_plan plan, void* workspace, size_t ws_bytes
 
 void libra_plan_destroy(libra_plan plan) {
   if (!plan) return;
-  if (plan->upload_done) {
-    (void)hipEventSynchronize(plan->upload_done);
-    (void)hipEventDestroy(plan->upload_done);
-  }
+  // The pinned image may still be the source of an enqueued copy: wait for that copy
+  // (only it, not the device) before the image goes back to the pool.
+  if (plan->upload_done) (void)hipEventSynchronize(plan->upload_done);
   {
     std::lock_guard<std::mutex> lk(g_ws.mu);
     for (auto it = g_ws.owner.begin(); it != g_ws.owner.end();)
       it = it->second == plan->id ? g_ws.owner.erase(it) : std::next(it);
   }
-  if (plan->pinned) (void)hipHostFree(plan->pinned);
+  staging_release(*plan);
   delete plan;
 }
 

@@ -34,8 +34,11 @@ struct Plan {
   uint64_t id = 0;          // process-unique, set at creation: which plan a workspace holds
 
   // Upload state (guarded by upload_mu: calls on one plan may come from several threads).
+  // The pinned image and the event come from the library's pool at plan creation and go
+  // back to it when the plan is destroyed; both stay null without a visible device.
   std::mutex upload_mu;
   void* pinned = nullptr;         // host staging copy of [units | writes | merges | xcd map]
+  size_t pinned_capacity = 0;
   hipEvent_t upload_done = nullptr;
 };
 

@@ -207,6 +207,14 @@ def test_layout_validation_codes():
     assert create(v_cache=fake + 2) == 1  # misaligned
 
 
+def _device_visible():
+    try:
+        import torch
+        return torch.cuda.is_available()
+    except Exception:
+        return False
+
+
 def test_call_validation_codes_before_any_launch():
     lib = libra.load()
     fake = 1 << 20
@@ -227,12 +235,17 @@ def test_call_validation_codes_before_any_launch():
     assert call(batch=3) == 1                      # batch differs from the plan
     assert call(hq=16) == 1                        # heads differ
     assert call(scale=float("nan")) == 1           # non-finite scale
+    assert call(scale=0.0) == 1 and call(scale=-0.088) == 1   # scale must be positive
+    assert "positive" in libra.libra_last_error()
     assert call(q=None) == 1                       # null q
     assert call(bt=None) == 1                      # null block table
     assert call(stride=6) == 1                     # 100 tokens need 7 pages
     assert call(ws_bytes=ws_need - 1) == 3         # short workspace
     assert call(ws=fake * 4 + 16) == 1             # misaligned workspace
     assert call(q=fake + 2) == 1                   # misaligned q
+    if not _device_visible():
+        # a plan built without a visible device has no pinned staging: it cannot run
+        assert call() == 1 and "visible HIP device" in libra.libra_last_error()
     aplan = libra.libra_splitkv_plan(libra.LIBRA_MODE_APPEND, 2, 8, 2, [40, 100], [1, 5], 8)
     assert lib.libra_decode_attn(lay, aplan, fake, fake, 7, 2, 8, 0.1, fake * 4, 1 << 20,
                                  fake * 8, None, None) == 1  # append plan in a decode call

@@ -1,7 +1,12 @@
-"""The library's host code (plans, reshard, cost evaluator, RolloutDP, prefix tree,
-routing) built with AddressSanitizer and UndefinedBehaviorSanitizer and fuzzed by a
-seeded C++ driver (tests/host_asan/driver.cpp).  Host code only: no device code is built
-and the driver calls no entry point that launches work."""
+"""The library's host code built with g++ (no device code), in two drivers:
+
+* plans, reshard, cost evaluator, RolloutDP, prefix tree and routing under
+  AddressSanitizer and UndefinedBehaviorSanitizer, fuzzed by a seeded C++ driver
+  (tests/host_asan/driver.cpp) that calls no entry point that launches work;
+* which entry points allocate (tests/host_asan/no_alloc_driver.cpp): the host code is
+  linked against a counting stand-in for the HIP runtime calls it makes
+  (tests/host_asan/fake_hip.cpp) and stubbed launches, and the driver asserts that
+  uploads, decode and append calls make no allocating runtime call once the plan exists."""
 import os
 import shutil
 import subprocess
@@ -29,3 +34,22 @@ def test_host_code_is_clean_under_asan_and_ubsan(tmp_path):
                ASAN_OPTIONS="detect_leaks=1")
     r = subprocess.run([exe], capture_output=True, text=True, env=env, timeout=600)
     assert r.returncode == 0 and "host fuzz ok" in r.stdout, (r.stdout + r.stderr)[-4000:]
+
+
+@pytest.mark.skipif(shutil.which("g++") is None or not os.path.isdir("/opt/rocm/include"),
+                    reason="needs g++ and the ROCm headers")
+def test_hot_calls_allocate_nothing_after_plan_creation(tmp_path):
+    exe = str(tmp_path / "no_alloc")
+    asan = os.path.join(ROOT, "tests", "host_asan")
+    cmd = ["g++", "-std=c++17", "-O1", "-g", "-fsanitize=address,undefined",
+           "-fno-sanitize-recover=all", "-fno-omit-frame-pointer", "-D__HIP_PLATFORM_AMD__",
+           "-DLIBRA_STUB_LAUNCH_OK", "-I/opt/rocm/include", "-I" + os.path.join(ROOT, "include"),
+           "-I" + CSRC, "-I" + asan]
+    cmd += [os.path.join(CSRC, f) for f in HOST_SOURCES]
+    cmd += [os.path.join(asan, f) for f in ("stubs.cpp", "fake_hip.cpp", "no_alloc_driver.cpp")]
+    cmd += ["-pthread", "-o", exe]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr[-4000:]
+    r = subprocess.run([exe], capture_output=True, text=True,
+                       env=dict(os.environ, ASAN_OPTIONS="detect_leaks=1"), timeout=300)
+    assert r.returncode == 0 and "no-alloc ok" in r.stdout, (r.stdout + r.stderr)[-4000:]
