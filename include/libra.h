@@ -341,6 +341,29 @@ libra_status libra_decode_attn(libra_kv_layout layout, libra_plan plan, const vo
                                void* out, float* lse, void* stream);
 
 /*
+ * For callers that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): libra_decode_attn with the library's
+ * static device scratch in place of a caller workspace.  Same arguments, layouts,
+ * kernels and results as libra_decode_attn without `workspace` / `ws_bytes`.
+ *
+ * The scratch is a fixed array of 8 MiB per GPU (every GPU the library runs on holds its
+ * own until the process ends); a plan whose libra_plan_workspace_bytes exceeds it is
+ * refused with LIBRA_E_WORKSPACE before anything is enqueued.  No call allocates
+ * (no hipMalloc, hipHostMalloc, hipFree or event creation); per-kernel timing is never
+ * recorded for it.  The first call on a device looks up the scratch's device address
+ * (hipGetSymbolAddress) with that device current; make one call before any capture.
+ * A call copies the plan's tables into the scratch (from the plan's pinned image) unless
+ * the scratch already holds that plan's tables, so repeated calls of one plan enqueue
+ * kernels only.  All calls on one GPU share its scratch: calls that may overlap on that
+ * GPU (other streams, other threads) race and must be ordered by the caller.  No kernel
+ * of this call needs the scratch zeroed; stale contents are overwritten before use.
+ */
+libra_status libra_decode_attn_noalloc(libra_kv_layout layout, libra_plan plan, const void* q,
+                                       const int32_t* block_table, int32_t bt_stride,
+                                       int32_t batch, int32_t num_q_heads, float scale, void* out,
+                                       float* lse, void* stream);
+
+/*
  * Append: sequence b adds C_b tokens (a tool-output chunk, or C_b = 1 for an ordinary
  * decode step) after P_b = L_b - C_b cached tokens, as when a tool returns and its
  * output is incorporated before decoding resumes (Sec. 5, Phase 2 and Step 3).  The

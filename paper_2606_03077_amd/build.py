@@ -23,7 +23,7 @@ LIB = os.path.join(PKG, "liblibra.so")
 ARCH = "gfx950"
 
 SOURCES = ["api.cpp", "plan.cpp", "migrate.cpp", "cost_model.cpp", "scheduler.cpp", "kv_layout.hip", "decode.hip", "merge.hip",
-           "chunk.hip", "xcd_weights.hip"]
+           "chunk.hip", "xcd_weights.hip", "scratch.hip"]
 
 # Packed-fp32 VALU forms are disabled for all device code (the host pass warns that it
 # does not know the feature; that is harmless).

@@ -115,6 +115,11 @@ struct WorkspaceOwners {
 WorkspaceOwners g_ws;
 std::atomic<uint64_t> g_next_plan_id{1};
 
+// Which plan's tables the static scratch of each device holds (0: none).  Plan ids are
+// never reused, so a destroyed plan's id can never match a live plan.
+constexpr int kMaxScratchOwners = 64;
+std::atomic<uint64_t> g_scratch_owner[kMaxScratchOwners] = {};
+
 bool holds_tables(const void* ws, uint64_t id) {
   std::lock_guard<std::mutex> lk(g_ws.mu);
   auto it = g_ws.owner.find(reinterpret_cast<uintptr_t>(ws));
@@ -256,23 +261,24 @@ libra_status check_call(const KvLayout* L, const Plan* P, int mode, const void* 
   return LIBRA_OK;
 }
 
-// Decode units, chunk units, then the merge of split rows, on one stream.
+// Decode units, chunk units, then the merge of split rows, on one stream.  `timed`
+// allows per-kernel timing events (which may create events while timing is enabled).
 libra_status launch_attention(const KvLayout& L, const Plan& P, void* ws, const void* q,
                               const int32_t* bt, int32_t stride, float scale, void* out,
-                              float* lse, hipStream_t s) {
+                              float* lse, hipStream_t s, bool timed = true) {
   hipError_t e;
   {
-    ProfScope ps(LIBRA_KERNEL_DECODE, s, P.info.n_single > 0);
+    ProfScope ps(LIBRA_KERNEL_DECODE, s, timed && P.info.n_single > 0);
     e = launch_decode(L, P, ws, q, bt, stride, scale, out, lse, s);
   }
   if (e != hipSuccess) return hip_error(e, "decode launch");
   {
-    ProfScope ps(LIBRA_KERNEL_CHUNK, s, P.info.n_chunk > 0);
+    ProfScope ps(LIBRA_KERNEL_CHUNK, s, timed && P.info.n_chunk > 0);
     e = launch_chunk(L, P, ws, q, bt, stride, scale, out, lse, s);
   }
   if (e != hipSuccess) return hip_error(e, "chunk launch");
   {
-    ProfScope ps(LIBRA_KERNEL_MERGE, s, merge_launches(P));
+    ProfScope ps(LIBRA_KERNEL_MERGE, s, timed && merge_launches(P));
     e = launch_merge(P, ws, out, lse, s);
   }
   return e == hipSuccess ? LIBRA_OK : hip_error(e, "merge launch");
@@ -552,6 +558,40 @@ libra_status libra_decode_attn(libra_kv_layout layout, libra_plan plan, const vo
   st = upload(*plan, workspace, ws_bytes, s, false);
   if (st != LIBRA_OK) return st;
   return launch_attention(*layout, *plan, workspace, q, block_table, bt_stride, scale, out, lse, s);
+}
+
+libra_status libra_decode_attn_noalloc(libra_kv_layout layout, libra_plan plan, const void* q,
+                                       const int32_t* block_table, int32_t bt_stride,
+                                       int32_t batch, int32_t num_q_heads, float scale, void* out,
+                                       float* lse, void* stream) {
+  libra_status st = check_call(layout, plan, LIBRA_MODE_DECODE, q, block_table, bt_stride, batch,
+                               num_q_heads, scale, out);
+  if (st != LIBRA_OK) return st;
+  if (plan->ws_bytes > scratch_capacity())
+    return set_error(LIBRA_E_WORKSPACE,
+                     "the plan needs " + std::to_string(plan->ws_bytes) +
+                         " bytes of scratch; the static scratch holds " +
+                         std::to_string(scratch_capacity()) +
+                         " bytes (libra_decode_attn takes a workspace of any size)");
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_error(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxScratchOwners)
+    return set_error(LIBRA_E_UNSUPPORTED, "device ordinal outside the scratch table (64 devices)");
+  void* ws = nullptr;
+  st = scratch_buffer(dev, &ws);
+  if (st != LIBRA_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  {
+    std::lock_guard<std::mutex> lk(plan->upload_mu);
+    if (g_scratch_owner[dev].load() != plan->id) {
+      st = enqueue_tables(*plan, ws, s);
+      if (st != LIBRA_OK) return st;
+      g_scratch_owner[dev].store(plan->id);
+    }
+  }
+  return launch_attention(*layout, *plan, ws, q, block_table, bt_stride, scale, out, lse, s,
+                          /*timed=*/false);
 }
 
 libra_status libra_append_attn(libra_kv_layout layout, libra_plan plan, const void* q,

@@ -78,4 +78,9 @@ hipError_t launch_chunk(const KvLayout& L, const Plan& P, void* ws, const void* 
                         const int32_t* bt, int32_t stride, float scale, void* out, float* lse,
                         hipStream_t s);
 
+// The static device scratch of libra_decode_attn_noalloc (csrc/scratch.hip): its size,
+// and its address on device `dev` (the calling thread's current device).
+size_t scratch_capacity();
+libra_status scratch_buffer(int dev, void** out);
+
 }  // namespace libra

@@ -34,7 +34,8 @@ EXPORTS = ("libra_status_string", "libra_last_error", "libra_kv_layout_create",
            "libra_xcd_read_weights", "libra_splitkv_plan", "libra_plan_get_units",
            "libra_plan_get_info",
            "libra_plan_workspace_bytes", "libra_plan_upload", "libra_plan_destroy",
-           "libra_decode_attn", "libra_append_attn", "libra_profile_enable",
+           "libra_decode_attn", "libra_decode_attn_noalloc", "libra_append_attn",
+           "libra_profile_enable",
            "libra_profile_collect", "libra_ce_fit", "libra_ce_mape", "libra_ce_poly_sum",
            "libra_rollout_dp", "libra_trie_create", "libra_trie_destroy", "libra_trie_insert",
            "libra_trie_lookup", "libra_route_bucket")
@@ -132,6 +133,8 @@ def load() -> ctypes.CDLL:
         "libra_plan_destroy": (None, [P]),
         "libra_decode_attn": (ctypes.c_int, [P, P, P, P, I32, I32, I32, ctypes.c_float, P, SZ,
                                              P, P, P]),
+        "libra_decode_attn_noalloc": (ctypes.c_int, [P, P, P, P, I32, I32, I32, ctypes.c_float,
+                                                     P, P, P]),
         "libra_append_attn": (ctypes.c_int, [P, P, P, P, P, P, I32, I32, I32, ctypes.c_float, P,
                                              SZ, P, P, P]),
         "libra_profile_enable": (ctypes.c_int, [ctypes.c_int]),
@@ -351,6 +354,14 @@ def libra_decode_attn(layout: int, plan: int, q, block_table, bt_stride: int, ba
     _check(load().libra_decode_attn(layout, plan, _ptr(q), _ptr(block_table), bt_stride, batch,
                                     num_q_heads, scale, _ptr(workspace), ws_bytes, _ptr(out),
                                     _ptr(lse), _stream(stream)), "libra_decode_attn")
+
+
+def libra_decode_attn_noalloc(layout: int, plan: int, q, block_table, bt_stride: int,
+                              batch: int, num_q_heads: int, scale: float, out, lse=None,
+                              stream=None):
+    _check(load().libra_decode_attn_noalloc(layout, plan, _ptr(q), _ptr(block_table), bt_stride,
+                                            batch, num_q_heads, scale, _ptr(out), _ptr(lse),
+                                            _stream(stream)), "libra_decode_attn_noalloc")
 
 
 def libra_append_attn(layout: int, plan: int, q, k_new, v_new, block_table, bt_stride: int,

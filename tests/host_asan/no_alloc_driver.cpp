@@ -112,6 +112,35 @@ int main() {
   CHECK(libra_decode_attn(lay, dec2, al16(m.q), reinterpret_cast<int32_t*>(al16(m.bt)), stride, B,
                           hq, 0.088f, ws1, wsb, al16(m.out), nullptr, nullptr) == LIBRA_OK);
   CHECK(g_fake_hip.allocations() == before_destroy.allocations());
+  // The static-scratch variant: no allocating call on its first call or later ones; its
+  // tables go to the scratch once per plan, and a plan too large for it is refused.
+  const FakeHipCounters before_static = g_fake_hip;
+  for (int it = 0; it < 3; ++it)
+    CHECK(libra_decode_attn_noalloc(lay, dec2, al16(m.q), reinterpret_cast<int32_t*>(al16(m.bt)),
+                                    stride, B, hq, 0.088f, al16(m.out), m.lse.data(),
+                                    nullptr) == LIBRA_OK);
+  CHECK(g_fake_hip.allocations() == before_static.allocations());
+  CHECK(g_fake_hip.memcpy_async - before_static.memcpy_async == 1);
+  CHECK(g_fake_hip.launches > before_static.launches);
+  CHECK(libra_decode_attn_noalloc(lay, dec2, al16(m.q), reinterpret_cast<int32_t*>(al16(m.bt)),
+                                  stride, B, hq, -1.f, al16(m.out), nullptr,
+                                  nullptr) == LIBRA_E_INVAL);
+  {
+    // 40 rows of 65,536 tokens cut into 64 splits each: 40 * 8 * 64 partial slots of
+    // 4 * 129 * 4 bytes, over 8 MiB of scratch.
+    std::vector<int32_t> big(40, 65536);
+    libra_plan_params pb{4096, 3, 1, 64, 0, {0, 0, 0, 0, 0, 0, 0, 0}};
+    libra_plan_desc db{LIBRA_MODE_DECODE, 40, hq, hkv};
+    libra_plan bigp = nullptr;
+    CHECK(libra_splitkv_plan(&db, big.data(), nullptr, &pb, &bigp) == LIBRA_OK);
+    CHECK(libra_plan_workspace_bytes(bigp) > (size_t(8) << 20));
+    const long copies = g_fake_hip.memcpy_async, launches = g_fake_hip.launches;
+    CHECK(libra_decode_attn_noalloc(lay, bigp, al16(m.q), reinterpret_cast<int32_t*>(al16(m.bt)),
+                                    65536 / 16, 40, hq, 0.088f, al16(m.out), nullptr,
+                                    nullptr) != LIBRA_OK);
+    CHECK(g_fake_hip.memcpy_async == copies && g_fake_hip.launches == launches);
+    libra_plan_destroy(bigp);
+  }
   libra_plan_destroy(dec2);
   libra_kv_layout_destroy(lay);
   std::printf("no-alloc ok: %ld launches, %ld table copies\n", g_fake_hip.launches,

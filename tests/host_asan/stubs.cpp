@@ -22,4 +22,11 @@ bool merge_launches(const Plan&) { return false; }
 hipError_t launch_chunk(const KvLayout&, const Plan&, void*, const void*, const int32_t*, int32_t, float, void*, float*, hipStream_t) { return LAUNCH_RESULT; }
 libra_status measure_xcd_weights(const void*, size_t, int, int32_t*, hipStream_t) { return LIBRA_E_HIP; }
 hipError_t launch_page_copy(const KvLayout&, const int32_t*, int64_t, void*, void*, bool, hipStream_t) { return LAUNCH_RESULT; }
+// The static device scratch lives in device code; here it is a host array.
+size_t scratch_capacity() { return size_t(8) << 20; }
+libra_status scratch_buffer(int, void** out) {
+  alignas(256) static unsigned char host_scratch[size_t(8) << 20];
+  *out = host_scratch;
+  return LIBRA_OK;
+}
 }  // namespace libra
