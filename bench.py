@@ -1,22 +1,28 @@
-"""Benchmark of ragged paged-KV decode attention on one MI355X.
+"""Benchmark of ragged paged-KV decode and append attention on one MI355X.
 
-    python bench.py [--gpus 1] [--steps 50] [--warmup 5] [--workload 7b]
+    python bench.py [--gpus 1] [--steps 50] [--warmup 5] [--workload longtail]
 
 One step = one decode-attention call (the split-KV decode kernel, then the log-sum-exp
-merge of split rows) over the whole synthetic batch, inputs resident in HBM.  Before each
-timed step an untimed 1 GiB fill evicts L2 and the 256 MB MALL, so every step reads its
-KV from HBM.  Each step is bracketed by HIP events on the stream the kernel runs on.
-The host-side split plan is built once per batch step and shared by all layers of a
-model; its time is reported separately (``plan_ms``) and is not part of a step.  Before
-planning, the per-XCD HBM read weights that the plan's slot placement takes are measured
-once on the flush buffer (``libra_xcd_read_weights``; ``--xcd-weights equal`` skips it).
+merge of split rows) over the whole synthetic batch, or one append call (cache write,
+decode rows, causal chunk tiles, merge), inputs resident in HBM.  Before each timed step
+an untimed 1 GiB fill evicts L2 and the 256 MB MALL, so every step reads its KV from HBM.
+Each step is bracketed by HIP events on the stream the kernels run on.  The host-side
+split plan is built once per batch step and shared by all layers of a model; its time is
+reported separately (``plan_ms``) and is not part of a step.  Before planning, the
+per-XCD HBM read weights that the plan's slot placement takes are measured once on the
+flush buffer (``libra_xcd_read_weights``; ``--xcd-weights equal`` skips it).
 
-Prints one JSON line (rank 0, N = 1):
+Prints one JSON line (rank 0, N = 1).  The headline is the long-tailed rollout batch
+(256 sequences, 32 query / 8 KV heads, 90% U[512, 4096] and 10% Pareto tails up to
+65,536 tokens):
   value = algorithmic KV bytes / mean step time (TB/s), plus decode tokens/s, the
-  roofline of the dominant kernel (decode_kernel against 8 TB/s HBM; for the append
-  workload chunk_kernel against 2.5 PFLOP/s bf16), and the fp64 oracle timed on the host
-  cores (``cpu_baseline``).  The dominant kernel's average duration comes from a second
-  timed pass in which the library brackets each of its kernels with HIP events.
+  roofline of the dominant kernel (decode_kernel against 8 TB/s HBM; chunk_kernel
+  against 2.5 PFLOP/s bf16 for append workloads), and the fp64 oracle timed on the
+  host cores (``cpu_baseline``).  The dominant kernel's average duration comes from a
+  second timed pass in which the library brackets each of its kernels with HIP events.
+  ``configs`` holds the same figures for the 7B-class batch, the straggler bucket, the
+  tool-output append batch (with its combined HBM / matrix-core roofline fraction) and
+  the 40,960-token recompute prefill, timed in the same run.
 """
 from __future__ import annotations
 
@@ -50,8 +56,9 @@ def algorithmic_bytes(batch) -> dict:
     o = rows * w.num_q_heads * 128 * 2
     lse = rows * w.num_q_heads * 4
     bt = int(((L + 15) // 16).sum()) * 4
-    return {"kv": kv, "q": q, "o": o, "lse": lse, "block_table": bt,
-            "total": kv + q + o + lse + bt}
+    kv_write = rows * w.num_kv_heads * 128 * 2 * 2 if w.append else 0   # new K and V
+    return {"kv": kv, "q": q, "o": o, "lse": lse, "block_table": bt, "kv_write": kv_write,
+            "total": kv + q + o + lse + bt + kv_write}
 
 
 def flops(batch) -> int:
@@ -85,8 +92,10 @@ def plan_sha(units: np.ndarray) -> str:
     return hashlib.sha256(np.ascontiguousarray(u).tobytes()).hexdigest()[:16]
 
 
-def traffic_from_profile(kernel: str, workload: str, units_sha: str):
-    """HBM bytes per launch of `kernel` from committed rocprofv3 counters.
+def counter_from_profile(kernel: str, workload: str, units_sha: str,
+                         field: str = "hbm_bytes_per_launch"):
+    """A committed rocprofv3 figure for `kernel` on `workload` (HBM bytes per launch, or
+    the matrix-core busy fraction).
 
     Null unless profiles/counters.json was taken on the current kernel source and on a
     plan with the same unit table.
@@ -99,49 +108,71 @@ def traffic_from_profile(kernel: str, workload: str, units_sha: str):
     e = c.get(kernel, {}).get(workload)
     if not e or e.get("source_sha") != kernel_source_sha(kernel) or e.get("plan_sha") != units_sha:
         return None
-    return e.get("hbm_bytes_per_launch")
-
-
-def _oracle_worker(args):
-    rows, = args
-    from threadpoolctl import threadpool_limits
-    import oracle
-    b = _ORACLE_BATCH
-    with threadpool_limits(1):
-        oracle.decode_ref(b.q, b.k_pages, b.v_pages, b.block_table, b.seq_lens, b.scale,
-                          batch_rows=rows)
-    return len(rows)
+    return e.get(field)
 
 
 _ORACLE_BATCH = None
 
 
+def _oracle_unit(bg):
+    """The fp64 oracle on one (sequence, KV head) unit of the batch; returns its K/V bytes."""
+    from threadpoolctl import threadpool_limits
+    import oracle
+    from paper_2606_03077_amd import workloads as wl
+    b, g = bg
+    u = wl.unit_batch(_ORACLE_BATCH, b, g)
+    with threadpool_limits(1):
+        if u.workload.append:
+            oracle.append_ref(u.q, u.k_new, u.v_new, u.k_pages, u.v_pages, u.block_table,
+                              u.seq_lens, u.q_lens, u.scale)
+        else:
+            oracle.decode_ref(u.q, u.k_pages, u.v_pages, u.block_table, u.seq_lens, u.scale)
+    return int(u.seq_lens[0]) * 128 * 2 * 2, int(u.q_lens[0])
+
+
 def cpu_baseline(batch, min_seconds: float = 10.0) -> dict:
-    """The fp64 oracle on the host cores: the whole batch, repeated for >= min_seconds."""
+    """The fp64 oracle on the host cores over a bounded sample of the batch.
+
+    Units are (sequence, KV head) pairs in a seeded random order, one per task, on a pool
+    of forked processes (BLAS single-threaded in each), until at least min_seconds have
+    passed; the rate is the K/V bytes of the finished units over the elapsed time."""
     import multiprocessing as mp
     global _ORACLE_BATCH
     _ORACLE_BATCH = batch
-    cores = len(os.sched_getaffinity(0))
-    cores = max(1, min(cores, 16))
-    B = len(batch.seq_lens)
-    order = np.argsort(-batch.seq_lens)  # longest first, one sequence per task
-    tasks = [([int(b)],) for b in order]
-    ctx = mp.get_context("fork")
-    kv_per_pass = algorithmic_bytes(batch)["kv"]
-    passes = 0
+    w = batch.workload
+    visible = len(os.sched_getaffinity(0))
+    # a one-GPU box allots this process a share of 16 host cores, whatever it shows
+    workers = max(1, min(visible, 16))
+    units = [(b, g) for b in range(len(batch.seq_lens)) for g in range(w.num_kv_heads)]
+    order = np.random.default_rng(0).permutation(len(units))
+    tasks = [units[i] for i in order]
+    done_bytes = done_units = done_rows = 0
     t0 = time.perf_counter()
-    with ctx.Pool(cores) as pool:
-        while True:
-            list(pool.imap_unordered(_oracle_worker, tasks))
-            passes += 1
-            el = time.perf_counter() - t0
-            if el >= min_seconds:
+    pool = mp.get_context("fork").Pool(workers)
+    try:
+        for _ in range(64):                      # passes over the batch, bounded
+            for nbytes, rows in pool.imap_unordered(_oracle_unit, tasks):
+                done_bytes += nbytes
+                done_units += 1
+                done_rows += rows
+                if time.perf_counter() - t0 >= min_seconds:
+                    break
+            if time.perf_counter() - t0 >= min_seconds:
                 break
-    rate = kv_per_pass * passes / el
-    return {"value": rate / 1e12, "unit": "TB/s", "cores": cores, "kind": "oracle",
-            "sample": f"whole {batch.workload.name} batch ({B} sequences) x {passes} passes, "
-                      f"{el:.1f} s, fp64 numpy, one process per core, one sequence per task",
-            "decode_tokens_per_s": B * passes / el}
+    finally:
+        pool.terminate()
+        pool.join()
+        _ORACLE_BATCH = None
+    el = time.perf_counter() - t0
+    kind = "append" if w.append else "decode"
+    return {"value": round(done_bytes / el / 1e12, 6), "unit": "TB/s", "cores": workers,
+            "kind": "oracle",
+            "host_cores_visible": visible,
+            "sample": f"{done_units} of {len(units)} (sequence, KV head) units of the "
+                      f"{w.name} batch in seeded random order ({done_units / len(units):.2f} "
+                      f"passes), {el:.1f} s, fp64 numpy {kind} oracle, one process per "
+                      f"core (the 16-core share of a one-GPU box; {visible} cores visible)",
+            "kv_bytes": done_bytes}
 
 
 PCIE_GEN5_X16_GBS = 64.0   # per direction, before protocol overhead
@@ -549,14 +580,214 @@ def bench_planner(args) -> dict:
     return result
 
 
+EXTRA_CONFIGS = ("7b", "straggler", "append", "prefill")
+
+
+def measure(name, args, torch, libra, wl, flush, xcd_weight, steps, warmup, cpu_seconds=0.0):
+    """Times one decode / append workload; returns its result fields (see the module
+    docstring) and, when cpu_seconds > 0, the oracle's rate on a sample of the same batch."""
+    dev = torch.device("cuda:0")
+    log(f"[bench] generating workload {name}")
+    t = time.perf_counter()
+    batch = wl.make_batch(name)
+    log(f"[bench] generated {name} in {time.perf_counter() - t:.1f} s")
+    w = batch.workload
+    P, Hkv = batch.k_pages.shape[0], batch.k_pages.shape[1]
+
+    k_cache = torch.empty(P * Hkv * 2048, dtype=torch.int16, device=dev)
+    v_cache = torch.empty_like(k_cache)
+    layout = libra.libra_kv_layout_create(k_cache, v_cache, P, Hkv)
+    k_log = torch.from_numpy(batch.k_pages.view(np.int16)).to(dev)
+    v_log = torch.from_numpy(batch.v_pages.view(np.int16)).to(dev)
+    libra.libra_kv_pack_pages(layout, k_log, v_log, 0, P)
+    torch.cuda.synchronize()
+    del k_log, v_log
+    bt = torch.from_numpy(batch.block_table).to(dev)
+    q = torch.from_numpy(batch.q.view(np.int16)).to(dev)
+    rows = batch.q.shape[0]
+    out = torch.empty((rows, w.num_q_heads, 128), dtype=torch.int16, device=dev)
+    lse = torch.empty((rows, w.num_q_heads), dtype=torch.float32, device=dev)
+    kn = vn = None
+    if w.append:
+        kn = torch.from_numpy(batch.k_new.view(np.int16)).to(dev)
+        vn = torch.from_numpy(batch.v_new.view(np.int16)).to(dev)
+
+    mode = libra.LIBRA_MODE_APPEND if w.append else libra.LIBRA_MODE_DECODE
+    ql = batch.q_lens.tolist() if w.append else None
+    B = len(batch.seq_lens)
+    plan_kw = dict(units_per_cu=args.units_per_cu, min_split_pages=args.min_split_pages,
+                   max_splits=args.max_splits, xcd_weight=xcd_weight)
+    plan_times = []
+    for _ in range(5):
+        t = time.perf_counter()
+        plan = libra.libra_splitkv_plan(mode, B, w.num_q_heads, Hkv, batch.seq_lens.tolist(),
+                                        ql, **plan_kw)
+        plan_times.append((time.perf_counter() - t) * 1e3)
+        libra.libra_plan_destroy(plan)
+    plan = libra.libra_splitkv_plan(mode, B, w.num_q_heads, Hkv, batch.seq_lens.tolist(), ql,
+                                    **plan_kw)
+    info = libra.libra_plan_get_info(plan)
+    ws = libra.alloc_workspace(plan)
+    stream = torch.cuda.current_stream()
+    libra.libra_plan_upload(plan, ws, stream=stream)
+
+    def step(p=plan):
+        if w.append:
+            libra.libra_append_attn(layout, p, q, kn, vn, bt, bt.shape[1], B, w.num_q_heads,
+                                    batch.scale, ws, out, lse, stream=stream)
+        else:
+            libra.libra_decode_attn(layout, p, q, bt, bt.shape[1], B, w.num_q_heads,
+                                    batch.scale, ws, out, lse, stream=stream)
+
+    log(f"[bench] {name}: warmup {warmup}")
+    for i in range(warmup):
+        flush.fill_(float(i))
+        step()
+    torch.cuda.synchronize()
+
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    log(f"[bench] {name}: timing {steps} steps")
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    for i in range(steps):
+        flush.fill_(float(i))           # untimed: evicts L2 / MALL
+        starts[i].record(stream)
+        step()
+        ends[i].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    times_ms = np.array([s.elapsed_time(e) for s, e in zip(starts, ends)])
+    mean_ms = float(times_ms.mean())
+    p10, p50, p90 = (float(x) for x in np.percentile(times_ms, [10, 50, 90]))
+
+    # Second timed pass: the library brackets each of its kernels with HIP events on the
+    # same stream, giving the dominant kernel's own average duration.
+    libra.libra_profile_enable(True)
+    libra.libra_profile_collect()
+    for i in range(steps):
+        flush.fill_(float(i))
+        step()
+    torch.cuda.synchronize()
+    ktimes = libra.libra_profile_collect()
+    libra.libra_profile_enable(False)
+    kernel_avg_ms = {k: ms / n for k, (ms, n) in ktimes.items() if n}
+
+    # A step that also builds, uploads and destroys its plan (host wall clock, synchronised):
+    # the per-step cost of a plan when every layer of a model shares it is plan_ms / layers.
+    with_plan = []
+    for i in range(min(steps, 10)):
+        flush.fill_(float(i))
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        p2 = libra.libra_splitkv_plan(mode, B, w.num_q_heads, Hkv, batch.seq_lens.tolist(), ql,
+                                      **plan_kw)
+        libra.libra_plan_upload(p2, ws, stream=stream)
+        step(p2)
+        libra.libra_plan_destroy(p2)
+        torch.cuda.synchronize()
+        with_plan.append((time.perf_counter() - t) * 1e3)
+    libra.libra_plan_upload(plan, ws, stream=stream)
+
+    ab = algorithmic_bytes(batch)
+    fl = flops(batch)
+    kv_tbs = ab["kv"] / (mean_ms * 1e-3) / 1e12
+    tokens_per_s = rows / (mean_ms * 1e-3)
+    units_sha = plan_sha(libra.libra_plan_get_units(plan))
+    if w.append:
+        # chunk rows dominate: a matrix-core bound contraction
+        ch = batch.q_lens > 1
+        sub = wl.Batch(w, batch.seq_lens[ch], batch.q_lens[ch], None, None, None, None, None,
+                       None, None, batch.scale)
+        kern = "chunk"
+        work = flops(sub)
+        achieved = work / (kernel_avg_ms[kern] * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4),
+                "traffic": counter_from_profile("chunk_kernel", name, units_sha),
+                "kernel": "chunk_kernel",
+                "algorithmic_flops_per_launch": work,
+                "mfma_busy": counter_from_profile("chunk_kernel", name, units_sha, "mfma_busy")}
+    else:
+        kern = "decode"
+        achieved = ab["total"] / (kernel_avg_ms[kern] * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                "traffic": counter_from_profile("decode_kernel", name, units_sha),
+                "kernel": "decode_kernel",
+                "algorithmic_bytes_per_launch": ab["total"]}
+    roof["kernel_avg_ms"] = round(kernel_avg_ms[kern], 5)
+    roof["other_kernels_avg_ms"] = {k: round(v, 5) for k, v in kernel_avg_ms.items() if k != kern}
+    # Whole-step roofline: the step cannot beat both its HBM bytes at 8 TB/s and its
+    # matrix-core flops at 2.5 PFLOP/s, whichever takes longer.
+    t_hbm = ab["total"] / (HBM_PEAK_GBS * 1e9) * 1e3
+    t_mfma = fl / (MFMA_BF16_PEAK_TFLOPS * 1e12) * 1e3
+    combined = {"t_roofline_ms": round(max(t_hbm, t_mfma), 5),
+                "t_hbm_ms": round(t_hbm, 5), "t_mfma_ms": round(t_mfma, 5),
+                "bound": "hbm" if t_hbm >= t_mfma else "mfma",
+                "t_step_ms": round(mean_ms, 5), "frac": round(max(t_hbm, t_mfma) / mean_ms, 4)}
+
+    result = {
+        "value": round(kv_tbs, 4),
+        "ms_per_step": round(mean_ms, 5),
+        "config": {"workload": f"{name}: {w.description}", "batch": B,
+                   "num_q_heads": w.num_q_heads, "num_kv_heads": Hkv, "head_dim": 128,
+                   "page_size": 16, "kv_tokens": int(batch.seq_lens.sum()),
+                   "query_rows": rows, "seed": w.seed},
+        "hbm_peak_frac": round(kv_tbs * 1e3 / HBM_PEAK_GBS, 4),
+        "decode_tokens_per_s": round(tokens_per_s, 1),
+        "step_ms_p10_p50_p90": [round(p10, 5), round(p50, 5), round(p90, 5)],
+        "timed_wall_s": round(wall, 4),
+        "plan_ms": round(float(np.median(plan_times)), 4),
+        "step_with_plan_upload_destroy_ms": round(float(np.median(with_plan)), 4),
+        "plan": dict({k: info[k] for k in ("n_units", "n_single", "n_chunk", "n_partial_slots",
+                                           "balanced", "chunk_pages", "num_cus")}, **plan_kw),
+        "algorithmic_bytes": ab["total"],
+        "flops": fl,
+        "roofline": roof,
+        "step_roofline": combined,
+    }
+    if cpu_seconds > 0:
+        log(f"[bench] {name}: timing the oracle on host cores (~{cpu_seconds:.0f} s)")
+        result["cpu_baseline"] = cpu_baseline(batch, cpu_seconds)
+    libra.libra_plan_destroy(plan)
+    libra.libra_kv_layout_destroy(layout)
+    del k_cache, v_cache, q, out, lse, kn, vn, bt, ws, batch
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return result
+
+
+def config_summary(r: dict) -> dict:
+    """The per-config block: step time, KV rate, and the dominant kernel's roofline."""
+    roof = r["roofline"]
+    out = {"workload": r["config"]["workload"], "ms_per_step": r["ms_per_step"],
+           "kv_TBps": r["value"], "hbm_peak_frac": r["hbm_peak_frac"],
+           "decode_tokens_per_s": r["decode_tokens_per_s"],
+           "step_ms_p10_p50_p90": r["step_ms_p10_p50_p90"],
+           "kernel": roof["kernel"], "kernel_avg_ms": roof["kernel_avg_ms"],
+           "kernel_frac": roof["frac"], "kernel_achieved": roof["achieved"],
+           "kernel_unit": roof["unit"], "traffic": roof["traffic"],
+           "other_kernels_avg_ms": roof["other_kernels_avg_ms"],
+           "algorithmic_bytes": r["algorithmic_bytes"], "flops": r["flops"],
+           "step_roofline": r["step_roofline"], "plan_ms": r["plan_ms"]}
+    if "mfma_busy" in roof:
+        out["mfma_busy"] = roof["mfma_busy"]
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="7b",
+    ap.add_argument("--workload", default="longtail",
                     choices=["tiny", "7b", "longtail", "straggler", "append", "prefill",
                              "migrate", "ce", "planner"])
+    ap.add_argument("--extra-configs", default=",".join(EXTRA_CONFIGS),
+                    help="decode / append workloads timed after the headline one and reported "
+                         "under 'configs' (comma-separated; empty for none)")
+    ap.add_argument("--extra-steps", type=int, default=20)
     ap.add_argument("--migrate-tokens", type=int, default=40960,
                     help="migrate workload: prefix length of the migrated request")
     ap.add_argument("--migrate-tp", default="1,2",
@@ -569,7 +800,7 @@ def main():
                     help="plan's per-XCD weights: 'measure' (libra_xcd_read_weights on the "
                          "flush buffer), 'equal', or 8 comma-separated integers")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy 3 times (the known-size "
                          "reference that rocprofv3 FETCH_SIZE / WRITE_SIZE are scaled by)")
@@ -613,33 +844,6 @@ def main():
         print(json.dumps(bench_ce(args, torch, libra)), flush=True)
         return
 
-    log(f"[bench] generating workload {args.workload}")
-    t = time.perf_counter()
-    batch = wl.make_batch(args.workload)
-    log(f"[bench] generated in {time.perf_counter() - t:.1f} s")
-    w = batch.workload
-    P, Hkv = batch.k_pages.shape[0], batch.k_pages.shape[1]
-
-    k_cache = torch.empty(P * Hkv * 2048, dtype=torch.int16, device=dev)
-    v_cache = torch.empty_like(k_cache)
-    layout = libra.libra_kv_layout_create(k_cache, v_cache, P, Hkv)
-    k_log = torch.from_numpy(batch.k_pages.view(np.int16)).to(dev)
-    v_log = torch.from_numpy(batch.v_pages.view(np.int16)).to(dev)
-    libra.libra_kv_pack_pages(layout, k_log, v_log, 0, P)
-    torch.cuda.synchronize()
-    del k_log, v_log
-    bt = torch.from_numpy(batch.block_table).to(dev)
-    q = torch.from_numpy(batch.q.view(np.int16)).to(dev)
-    rows = batch.q.shape[0]
-    out = torch.empty((rows, w.num_q_heads, 128), dtype=torch.int16, device=dev)
-    lse = torch.empty((rows, w.num_q_heads), dtype=torch.float32, device=dev)
-    kn = vn = None
-    if w.append:
-        kn = torch.from_numpy(batch.k_new.view(np.int16)).to(dev)
-        vn = torch.from_numpy(batch.v_new.view(np.int16)).to(dev)
-
-    mode = libra.LIBRA_MODE_APPEND if w.append else libra.LIBRA_MODE_DECODE
-    ql = batch.q_lens.tolist() if w.append else None
     flush = torch.empty(args.flush_mib * (1 << 20) // 4, dtype=torch.float32, device=dev)
     if args.xcd_weights == "measure":
         calib = flush if flush.numel() * 4 >= (1 << 30) else torch.empty(1 << 30, dtype=torch.uint8, device=dev)
@@ -650,127 +854,32 @@ def main():
         xcd_weight = [0] * 8
     else:
         xcd_weight = [int(x) for x in args.xcd_weights.split(",")]
-    plan_kw = dict(units_per_cu=args.units_per_cu, min_split_pages=args.min_split_pages,
-                   max_splits=args.max_splits, xcd_weight=xcd_weight)
-    plan_times = []
-    for _ in range(5):
-        t = time.perf_counter()
-        plan = libra.libra_splitkv_plan(mode, len(batch.seq_lens), w.num_q_heads, Hkv,
-                                        batch.seq_lens.tolist(), ql, **plan_kw)
-        plan_times.append((time.perf_counter() - t) * 1e3)
-        libra.libra_plan_destroy(plan)
-    plan = libra.libra_splitkv_plan(mode, len(batch.seq_lens), w.num_q_heads, Hkv,
-                                    batch.seq_lens.tolist(), ql, **plan_kw)
-    info = libra.libra_plan_get_info(plan)
-    ws = libra.alloc_workspace(plan)
-    stream = torch.cuda.current_stream()
-    libra.libra_plan_upload(plan, ws, stream=stream)
 
-    def step():
-        if w.append:
-            libra.libra_append_attn(layout, plan, q, kn, vn, bt, bt.shape[1], len(batch.seq_lens),
-                                    w.num_q_heads, batch.scale, ws, out, lse, stream=stream)
-        else:
-            libra.libra_decode_attn(layout, plan, q, bt, bt.shape[1], len(batch.seq_lens),
-                                    w.num_q_heads, batch.scale, ws, out, lse, stream=stream)
-
-    log(f"[bench] warmup {args.warmup}")
-    for i in range(args.warmup):
-        flush.fill_(float(i))
-        step()
-    torch.cuda.synchronize()
-
-    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
-    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
-    log(f"[bench] timing {args.steps} steps")
-    torch.cuda.synchronize()
-    wall0 = time.perf_counter()
-    for i in range(args.steps):
-        flush.fill_(float(i))           # untimed: evicts L2 / MALL
-        starts[i].record(stream)
-        step()
-        ends[i].record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - wall0
-    times_ms = np.array([s.elapsed_time(e) for s, e in zip(starts, ends)])
-    mean_ms = float(times_ms.mean())
-    p10, p50, p90 = (float(x) for x in np.percentile(times_ms, [10, 50, 90]))
-
-    # Second timed pass: the library brackets each of its kernels with HIP events on the
-    # same stream, giving the dominant kernel's own average duration.
-    libra.libra_profile_enable(True)
-    libra.libra_profile_collect()
-    for i in range(args.steps):
-        flush.fill_(float(i))
-        step()
-    torch.cuda.synchronize()
-    ktimes = libra.libra_profile_collect()
-    libra.libra_profile_enable(False)
-    kernel_avg_ms = {k: ms / n for k, (ms, n) in ktimes.items() if n}
-
-    ab = algorithmic_bytes(batch)
-    fl = flops(batch)
-    kv_tbs = ab["kv"] / (mean_ms * 1e-3) / 1e12
-    tokens_per_s = rows / (mean_ms * 1e-3)
-    if w.append:
-        # chunk rows dominate: a matrix-core bound contraction
-        ch = batch.q_lens > 1
-        sub = wl.Batch(w, batch.seq_lens[ch], batch.q_lens[ch], None, None, None, None, None,
-                       None, None, batch.scale)
-        kern = "chunk"
-        work = flops(sub)
-        achieved = work / (kernel_avg_ms[kern] * 1e-3) / 1e12
-        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4),
-                "traffic": traffic_from_profile("chunk_kernel", args.workload,
-                                                plan_sha(libra.libra_plan_get_units(plan))),
-                "kernel": "chunk_kernel",
-                "algorithmic_flops_per_launch": work}
-    else:
-        kern = "decode"
-        achieved = ab["total"] / (kernel_avg_ms[kern] * 1e-3) / 1e9
-        roof = {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                "traffic": traffic_from_profile("decode_kernel", args.workload,
-                                                plan_sha(libra.libra_plan_get_units(plan))),
-                "kernel": "decode_kernel",
-                "algorithmic_bytes_per_launch": ab["total"]}
-    roof["kernel_avg_ms"] = round(kernel_avg_ms[kern], 5)
-    roof["other_kernels_avg_ms"] = {k: round(v, 5) for k, v in kernel_avg_ms.items() if k != kern}
-
+    head = measure(args.workload, args, torch, libra, wl, flush, xcd_weight, args.steps,
+                   args.warmup, 0.0 if args.no_cpu_baseline else args.cpu_seconds)
     result = {
         "metric": "KV TB/s and % HBM peak for ragged paged decode attn; decode tokens/s",
-        "value": round(kv_tbs, 4),
+        "value": head["value"],
         "unit": "TB/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(mean_ms, 5),
+        "ms_per_step": head["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic (seeded; lengths and values as documented in workloads.py)",
-        "config": {"workload": f"{args.workload}: {w.description}", "batch": len(batch.seq_lens),
-                   "num_q_heads": w.num_q_heads, "num_kv_heads": Hkv, "head_dim": 128,
-                   "page_size": 16, "kv_tokens": int(batch.seq_lens.sum()),
-                   "query_rows": rows, "seed": w.seed},
-        "hbm_peak_frac": round(kv_tbs * 1e3 / HBM_PEAK_GBS, 4),
-        "decode_tokens_per_s": round(tokens_per_s, 1),
-        "step_ms_p10_p50_p90": [round(p10, 5), round(p50, 5), round(p90, 5)],
-        "timed_wall_s": round(wall, 4),
-        "plan_ms": round(float(np.median(plan_times)), 4),
-        "plan": dict({k: info[k] for k in ("n_units", "n_single", "n_chunk", "n_partial_slots", "balanced",
-                                           "chunk_pages", "num_cus")}, **plan_kw),
-        "algorithmic_bytes": ab["total"],
-        "flops": fl,
-        "roofline": roof,
     }
-    if not args.no_cpu_baseline:
-        log(f"[bench] timing the oracle on host cores (~{args.cpu_seconds:.0f} s)")
-        result["cpu_baseline"] = cpu_baseline(batch, args.cpu_seconds)
-    libra.libra_plan_destroy(plan)
-    libra.libra_kv_layout_destroy(layout)
+    result.update({k: v for k, v in head.items() if k not in ("value", "ms_per_step")})
+    extras = [x for x in args.extra_configs.split(",") if x and x != args.workload]
+    if extras:
+        result["configs"] = {}
+        for name in extras:
+            r = measure(name, args, torch, libra, wl, flush, xcd_weight, args.extra_steps,
+                        min(args.warmup, 3))
+            result["configs"][name] = config_summary(r)
+            log(f"[bench] {name}: {r['ms_per_step']:.4f} ms/step, {r['value']:.3f} KV TB/s")
     print(json.dumps(result), flush=True)
 
 

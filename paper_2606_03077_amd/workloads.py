@@ -295,6 +295,39 @@ def custom_batch(seq_lens, q_lens=None, num_q_heads=8, num_kv_heads=2, seed=0,
     return build_batch(w, seq_lens, q_lens, rng, spare_frac=spare_frac, poison=poison)
 
 
+def unit_batch(batch: Batch, b: int, g: int) -> Batch:
+    """Sequence b with KV head g (and the G query heads that read it) as a batch of its
+    own, its pages renamed 0..n-1 in logical order.  Pure data movement (no arithmetic):
+    a renamed page pool and a head slice hold the same tokens, so attention over the unit
+    equals that slice of attention over the batch.  Used to run the oracle on a batch in
+    parallel host processes."""
+    w = batch.workload
+    G = w.num_q_heads // w.num_kv_heads
+    L = int(batch.seq_lens[b])
+    n = (L + PAGE - 1) // PAGE
+    if n:
+        ids = batch.block_table[b, :n]
+        kp = np.ascontiguousarray(batch.k_pages[ids, g:g + 1])
+        vp = np.ascontiguousarray(batch.v_pages[ids, g:g + 1])
+    else:
+        kp = np.full((1, 1, PAGE, HEAD_DIM), BF16_NAN, np.uint16)
+        vp = kp.copy()
+    bt = np.arange(max(n, 1), dtype=np.int32)[None, :]
+    heads = slice(g * G, (g + 1) * G)
+    if w.append:
+        r0, r1 = int(batch.cu_q_lens[b]), int(batch.cu_q_lens[b + 1])
+        q = np.ascontiguousarray(batch.q[r0:r1, heads])
+        kn = np.ascontiguousarray(batch.k_new[r0:r1, g:g + 1])
+        vn = np.ascontiguousarray(batch.v_new[r0:r1, g:g + 1])
+    else:
+        q = np.ascontiguousarray(batch.q[b:b + 1, heads])
+        kn = vn = None
+    sub = dataclasses.replace(w, batch=1, num_q_heads=G, num_kv_heads=1)
+    C = int(batch.q_lens[b])
+    return Batch(sub, batch.seq_lens[b:b + 1].copy(), batch.q_lens[b:b + 1].copy(),
+                 np.array([0, C], np.int32), bt, kp, vp, q, kn, vn, batch.scale)
+
+
 # --- synthetic agentic trajectories (stand-ins for the paper's rollout logs) ---------
 
 def tool_state(tool_type: int, large: bool, failure: bool) -> int:

@@ -143,43 +143,11 @@ def assert_parity(o, lse, ro, rl, rows=None, label=""):
 _POOL_BATCH = None
 
 
-def one_unit(batch: wl.Batch, b: int, g: int) -> wl.Batch:
-    """Sequence b with KV head g (and the query heads that read it) as a batch of its own,
-    its pages renamed 0..n-1.  Both steps only move data: the oracle's pins show that
-    renaming pages (page-permutation invariance) and taking a head slice (head-shard
-    equivalence) leave its results unchanged."""
-    w = batch.workload
-    G = w.num_q_heads // w.num_kv_heads
-    L = int(batch.seq_lens[b])
-    n = (L + 15) // 16
-    if n:
-        ids = batch.block_table[b, :n]
-        kp = np.ascontiguousarray(batch.k_pages[ids, g:g + 1])
-        vp = np.ascontiguousarray(batch.v_pages[ids, g:g + 1])
-    else:
-        kp = np.full((1, 1, 16, 128), wl.BF16_NAN, np.uint16)
-        vp = kp.copy()
-    bt = np.arange(max(n, 1), dtype=np.int32)[None, :]
-    heads = slice(g * G, (g + 1) * G)
-    if w.append:
-        r0, r1 = int(batch.cu_q_lens[b]), int(batch.cu_q_lens[b + 1])
-        q = np.ascontiguousarray(batch.q[r0:r1, heads])
-        kn = np.ascontiguousarray(batch.k_new[r0:r1, g:g + 1])
-        vn = np.ascontiguousarray(batch.v_new[r0:r1, g:g + 1])
-    else:
-        q = np.ascontiguousarray(batch.q[b:b + 1, heads])
-        kn = vn = None
-    sub = wl.dataclasses.replace(w, batch=1, num_q_heads=G, num_kv_heads=1)
-    C = int(batch.q_lens[b])
-    return wl.Batch(sub, batch.seq_lens[b:b + 1].copy(), batch.q_lens[b:b + 1].copy(),
-                    np.array([0, C], np.int32), bt, kp, vp, q, kn, vn, batch.scale)
-
-
 def _unit_task(bg):
     from threadpoolctl import threadpool_limits
     import oracle
     b, g = bg
-    u = one_unit(_POOL_BATCH, b, g)
+    u = wl.unit_batch(_POOL_BATCH, b, g)
     with threadpool_limits(1):
         if u.workload.append:
             o, l, _, _ = oracle.append_ref(u.q, u.k_new, u.v_new, u.k_pages, u.v_pages,
