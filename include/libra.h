@@ -23,8 +23,10 @@
  *   No entry point synchronises the device or allocates device memory, except
  *   libra_xcd_read_weights (set-up) and libra_plan_destroy, which waits for the plan's
  *   own pending table upload (an event, not the device).  libra_splitkv_plan takes the
- *   plan's pinned host image of its tables and an upload event from a library-owned pool
- *   (allocating them only when the pool has none free); libra_plan_destroy returns them
+ *   plan's pinned host image of its tables and its events from a library-owned pool
+ *   (allocating them only when the pool has none free), and the first plan with both
+ *   single-token and chunk rows creates the device's auxiliary stream (default
+ *   priority, kept until the process ends); libra_plan_destroy returns image and events
  *   to the pool.  Decode, append and upload calls allocate nothing.
  * - Host-only entry points (plan construction, cost evaluator, RolloutDP, prefix tree,
  *   routing, libra_kv_reshard_host) touch no GPU; the reshard may use up to 8 host
@@ -374,6 +376,13 @@ libra_status libra_decode_attn_noalloc(libra_kv_layout layout, libra_plan plan, 
  * sum_{b' < b} C_b'.  k_new, v_new: device bf16 [sum C_b][num_kv_heads][128].  lse:
  * device float32 [sum C_b][num_q_heads] or NULL.  The block table must already map the
  * pages of positions [0, L_b).  The plan must be an append plan for the same shapes.
+ *
+ * When the plan has both single-token rows and chunk rows, the chunk tiles are
+ * launched on `stream` and the single-token rows on the library's auxiliary stream of
+ * the current device, forked from `stream` after the cache write and joined back before
+ * the split merge (events only): the matrix-core bound chunk tiles and the HBM-bound
+ * decode rows then share the device.  Work enqueued on `stream` after the call starts
+ * after both.  Under HIP graph capture this is the usual fork / join, captured as such.
  */
 libra_status libra_append_attn(libra_kv_layout layout, libra_plan plan, const void* q,
                                const void* k_new, const void* v_new, const int32_t* block_table,

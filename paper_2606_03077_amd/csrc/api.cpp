@@ -163,15 +163,25 @@ libra_status staging_acquire(Plan& P) {
       P.pinned_capacity = cap;
     }
   }
-  if (!g_staging.events.empty()) {
-    P.upload_done = g_staging.events.back();
-    g_staging.events.pop_back();
-  } else {
-    hipError_t e = hipEventCreateWithFlags(&P.upload_done, hipEventDisableTiming);
-    if (e != hipSuccess) {
-      P.upload_done = nullptr;
-      return hip_error(e, "hipEventCreate(plan upload)");
+  auto take_event = [](hipEvent_t* ev) -> libra_status {
+    if (!g_staging.events.empty()) {
+      *ev = g_staging.events.back();
+      g_staging.events.pop_back();
+      return LIBRA_OK;
     }
+    hipError_t e = hipEventCreateWithFlags(ev, hipEventDisableTiming);
+    if (e != hipSuccess) {
+      *ev = nullptr;
+      return hip_error(e, "hipEventCreate(plan)");
+    }
+    return LIBRA_OK;
+  };
+  libra_status st = take_event(&P.upload_done);
+  if (st != LIBRA_OK) return st;
+  if (P.info.n_single > 0 && P.info.n_chunk > 0) {
+    st = take_event(&P.fork_ev);
+    if (st == LIBRA_OK) st = take_event(&P.join_ev);
+    if (st != LIBRA_OK) return st;
   }
   return LIBRA_OK;
 }
@@ -179,9 +189,41 @@ libra_status staging_acquire(Plan& P) {
 void staging_release(Plan& P) {
   std::lock_guard<std::mutex> lk(g_staging.mu);
   if (P.pinned) g_staging.images.emplace_back(P.pinned_capacity, P.pinned);
-  if (P.upload_done) g_staging.events.push_back(P.upload_done);
+  for (hipEvent_t* ev : {&P.upload_done, &P.fork_ev, &P.join_ev}) {
+    if (*ev) g_staging.events.push_back(*ev);
+    *ev = nullptr;
+  }
   P.pinned = nullptr;
-  P.upload_done = nullptr;
+}
+
+// One auxiliary stream per device (default priority, non-blocking), created with the
+// first plan that has both decode rows and chunk tiles, and kept until the process ends.
+constexpr int kMaxAuxDevices = 64;
+std::mutex g_aux_mu;
+hipStream_t g_aux_stream[kMaxAuxDevices] = {};
+
+libra_status ensure_aux_stream() {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_error(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxAuxDevices) return LIBRA_OK;  // such devices run sequentially
+  std::lock_guard<std::mutex> lk(g_aux_mu);
+  if (!g_aux_stream[dev]) {
+    e = hipStreamCreateWithFlags(&g_aux_stream[dev], hipStreamNonBlocking);
+    if (e != hipSuccess) {
+      g_aux_stream[dev] = nullptr;
+      return hip_error(e, "hipStreamCreate(auxiliary)");
+    }
+  }
+  return LIBRA_OK;
+}
+
+// The current device's auxiliary stream, or null if it has none (then run sequentially).
+hipStream_t aux_stream() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxAuxDevices) return nullptr;
+  std::lock_guard<std::mutex> lk(g_aux_mu);
+  return g_aux_stream[dev];
 }
 
 // Fills the plan's pinned image with its tables (at plan creation).
@@ -261,22 +303,55 @@ libra_status check_call(const KvLayout* L, const Plan* P, int mode, const void* 
   return LIBRA_OK;
 }
 
-// Decode units, chunk units, then the merge of split rows, on one stream.  `timed`
-// allows per-kernel timing events (which may create events while timing is enabled).
+// Decode units, chunk units, then the merge of split rows.  `timed` allows per-kernel
+// timing events (which may create events while timing is enabled).  When the plan has
+// both decode rows and chunk tiles, the chunk launch goes first on `s` and the decode
+// launch on the device's auxiliary stream, forked from `s` after everything enqueued
+// before and joined back before the merge: the dispatcher then fills the CUs that the
+// matrix-core bound chunk tiles free with the HBM-bound decode rows as they come.
+std::mutex g_fork_mu;  // record / wait pairs of concurrent callers must not interleave
+
 libra_status launch_attention(const KvLayout& L, const Plan& P, void* ws, const void* q,
                               const int32_t* bt, int32_t stride, float scale, void* out,
                               float* lse, hipStream_t s, bool timed = true) {
   hipError_t e;
-  {
-    ProfScope ps(LIBRA_KERNEL_DECODE, s, timed && P.info.n_single > 0);
-    e = launch_decode(L, P, ws, q, bt, stride, scale, out, lse, s);
+  hipStream_t s2 = nullptr;
+  if (P.info.n_single > 0 && P.info.n_chunk > 0 && P.fork_ev && P.join_ev) s2 = aux_stream();
+  if (s2) {
+    {
+      std::lock_guard<std::mutex> lk(g_fork_mu);
+      e = hipEventRecord(P.fork_ev, s);
+      if (e == hipSuccess) e = hipStreamWaitEvent(s2, P.fork_ev, 0);
+    }
+    if (e != hipSuccess) return hip_error(e, "forking the decode rows");
+    {
+      ProfScope ps(LIBRA_KERNEL_CHUNK, s, timed);
+      e = launch_chunk(L, P, ws, q, bt, stride, scale, out, lse, s);
+    }
+    if (e != hipSuccess) return hip_error(e, "chunk launch");
+    {
+      ProfScope ps(LIBRA_KERNEL_DECODE, s2, timed);
+      e = launch_decode(L, P, ws, q, bt, stride, scale, out, lse, s2);
+    }
+    if (e != hipSuccess) return hip_error(e, "decode launch");
+    {
+      std::lock_guard<std::mutex> lk(g_fork_mu);
+      e = hipEventRecord(P.join_ev, s2);
+      if (e == hipSuccess) e = hipStreamWaitEvent(s, P.join_ev, 0);
+    }
+    if (e != hipSuccess) return hip_error(e, "joining the decode rows");
+  } else {
+    {
+      ProfScope ps(LIBRA_KERNEL_DECODE, s, timed && P.info.n_single > 0);
+      e = launch_decode(L, P, ws, q, bt, stride, scale, out, lse, s);
+    }
+    if (e != hipSuccess) return hip_error(e, "decode launch");
+    {
+      ProfScope ps(LIBRA_KERNEL_CHUNK, s, timed && P.info.n_chunk > 0);
+      e = launch_chunk(L, P, ws, q, bt, stride, scale, out, lse, s);
+    }
+    if (e != hipSuccess) return hip_error(e, "chunk launch");
   }
-  if (e != hipSuccess) return hip_error(e, "decode launch");
-  {
-    ProfScope ps(LIBRA_KERNEL_CHUNK, s, timed && P.info.n_chunk > 0);
-    e = launch_chunk(L, P, ws, q, bt, stride, scale, out, lse, s);
-  }
-  if (e != hipSuccess) return hip_error(e, "chunk launch");
   {
     ProfScope ps(LIBRA_KERNEL_MERGE, s, timed && merge_launches(P));
     e = launch_merge(P, ws, out, lse, s);
@@ -490,6 +565,7 @@ libra_status libra_splitkv_plan(const libra_plan_desc* desc, const int32_t* seq_
     (void)hipGetLastError();
   } else {
     st = staging_acquire(*P);
+    if (st == LIBRA_OK && P->fork_ev) st = ensure_aux_stream();
     if (st != LIBRA_OK) {
       staging_release(*P);
       delete P;

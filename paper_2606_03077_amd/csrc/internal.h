@@ -40,6 +40,10 @@ struct Plan {
   void* pinned = nullptr;         // host staging copy of [units | writes | merges | xcd map]
   size_t pinned_capacity = 0;
   hipEvent_t upload_done = nullptr;
+  // Plans with both decode rows and chunk tiles run the two launches concurrently: the
+  // decode rows on the device's auxiliary stream, forked from and joined back to the
+  // caller's stream by these events (from the pool; null otherwise).
+  hipEvent_t fork_ev = nullptr, join_ev = nullptr;
 };
 
 struct KvLayout {

@@ -75,6 +75,15 @@ hipError_t hipEventElapsedTime(float* ms, hipEvent_t, hipEvent_t) {
   *ms = 0.f;
   return hipSuccess;
 }
+hipError_t hipStreamCreateWithFlags(hipStream_t* st, unsigned int) {
+  ++g_fake_hip.stream_create;
+  *st = reinterpret_cast<hipStream_t>(new int(0));
+  return hipSuccess;
+}
+hipError_t hipStreamWaitEvent(hipStream_t, hipEvent_t, unsigned int) {
+  ++g_fake_hip.stream_wait;
+  return hipSuccess;
+}
 hipError_t hipMemcpyAsync(void* dst, const void* src, size_t n, hipMemcpyKind, hipStream_t) {
   ++g_fake_hip.memcpy_async;
   std::memcpy(dst, src, n);

@@ -71,7 +71,10 @@ int main() {
   CHECK(libra_splitkv_plan(&dd, lens, nullptr, &p, &dec) == LIBRA_OK);
   CHECK(libra_splitkv_plan(&da, lens, qlens, &p, &app) == LIBRA_OK);
   CHECK(g_fake_hip.host_malloc - before_plans.host_malloc == 2);
-  CHECK(g_fake_hip.event_create - before_plans.event_create == 2);
+  // one upload event each; the append plan (decode rows and chunk tiles) also takes its
+  // fork / join events and creates the device's auxiliary stream
+  CHECK(g_fake_hip.event_create - before_plans.event_create == 4);
+  CHECK(g_fake_hip.stream_create - before_plans.stream_create == 1);
 
   const size_t wsd = libra_plan_workspace_bytes(dec), wsa = libra_plan_workspace_bytes(app);
   Buffers w1, w2;
@@ -94,6 +97,7 @@ int main() {
   const FakeHipCounters& after = g_fake_hip;
   CHECK(after.allocations() == before.allocations());
   CHECK(after.launches > before.launches);          // the calls did reach their launches
+  CHECK(after.stream_wait - before.stream_wait == 6);  // fork and join of 3 append calls
   CHECK(after.memcpy_async - before.memcpy_async >= 4);  // tables re-uploaded on turns
   // The uploaded table image is the plan's unit table.
   const int32_t* units = nullptr;
