@@ -872,6 +872,24 @@ def main():
         "data": "synthetic (seeded; lengths and values as documented in workloads.py)",
     }
     result.update({k: v for k, v in head.items() if k not in ("value", "ms_per_step")})
+    # The chip's achievable streaming read rate over as many bytes as the headline step
+    # reads, beside the 8 TB/s figure: one pass timed to completion (ramp and tail
+    # included, like any kernel), and the rate while every CU reads (fixed interval).
+    nbytes = max(1 << 30, (int(head["algorithmic_bytes"]) + (1 << 20) - 1) >> 20 << 20)
+    rbuf = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    interval, completion = libra.libra_hbm_read_rate(rbuf, reps=5,
+                                                     stream=torch.cuda.current_stream())
+    del rbuf
+    torch.cuda.empty_cache()
+    result["hbm_read_ceiling"] = {"completion_GBps": round(completion, 1),
+                                  "interval_GBps": round(interval, 1), "bytes": nbytes,
+                                  "kernel": "16-byte non-temporal loads, 2048 workgroups "
+                                            "(libra_hbm_read_rate)"}
+    if result["roofline"]["unit"] == "GB/s":
+        result["roofline"]["frac_of_measured_read_ceiling"] = round(
+            result["roofline"]["achieved"] / completion, 4)
+    log(f"[bench] HBM read ceiling: {completion:.0f} GB/s to completion, {interval:.0f} GB/s "
+        f"over a fixed interval ({nbytes / 1e9:.2f} GB)")
     extras = [x for x in args.extra_configs.split(",") if x and x != args.workload]
     if extras:
         result["configs"] = {}

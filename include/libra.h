@@ -290,6 +290,18 @@ libra_status libra_splitkv_plan(const libra_plan_desc* desc, const int32_t* seq_
  * and waits for `stream`: for set-up, not for graph capture. */
 libra_status libra_xcd_read_weights(const void* buf, size_t bytes, int32_t reps,
                                     int32_t* weights, void* stream);
+/* Measures the device's achievable HBM read rate, the ceiling a bandwidth-bound kernel is
+ * compared with beside the vendor's peak.  `buf` (device memory of any contents, 256-byte
+ * aligned, bytes >= 1 GiB, only read) is cut into 2048 contiguous blocks, one per
+ * workgroup of 256 threads (8 per CU on 256 CUs), each streamed with 16-byte non-temporal
+ * loads, four in flight per lane.  completion_gbps: one pass over the whole buffer timed
+ * by events around the launch (ramp and tail included, as for any kernel that must finish
+ * its bytes); interval_gbps: the loads issued while every workgroup reads for 100 us of
+ * the device's constant clock.  Each is the median of `reps` runs (1 <= reps <= 100)
+ * after one warm-up run.  Allocates 64 KiB of device memory for the call and waits for
+ * `stream`: for set-up and measurement, not for graph capture. */
+libra_status libra_hbm_read_rate(const void* buf, size_t bytes, int32_t reps,
+                                 double* interval_gbps, double* completion_gbps, void* stream);
 /* Host view of the unit table (valid until libra_plan_destroy). */
 libra_status libra_plan_get_units(libra_plan plan, const int32_t** units_host, int32_t* n_units);
 libra_status libra_plan_get_info(libra_plan plan, libra_plan_info* info);

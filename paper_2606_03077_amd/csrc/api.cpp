@@ -587,6 +587,18 @@ libra_status libra_xcd_read_weights(const void* buf, size_t bytes, int32_t reps,
   return measure_xcd_weights(buf, bytes, reps, weights, static_cast<hipStream_t>(stream));
 }
 
+libra_status libra_hbm_read_rate(const void* buf, size_t bytes, int32_t reps,
+                                 double* interval_gbps, double* completion_gbps, void* stream) {
+  if (!buf || !interval_gbps || !completion_gbps)
+    return set_error(LIBRA_E_INVAL, "buf or an output is NULL");
+  if (reinterpret_cast<uintptr_t>(buf) % kWorkspaceAlign)
+    return set_error(LIBRA_E_INVAL, "buf must be 256-byte aligned");
+  if (bytes < (size_t(1) << 30)) return set_error(LIBRA_E_INVAL, "buf must hold at least 1 GiB");
+  if (reps < 1 || reps > 100) return set_error(LIBRA_E_INVAL, "reps must lie in [1, 100]");
+  return measure_hbm_read_rate(buf, bytes, reps, interval_gbps, completion_gbps,
+                               static_cast<hipStream_t>(stream));
+}
+
 libra_status libra_plan_get_units(libra_plan plan, const int32_t** units_host, int32_t* n_units) {
   if (!plan || !units_host || !n_units) return set_error(LIBRA_E_INVAL, "NULL argument");
   *units_host = plan->units.data();

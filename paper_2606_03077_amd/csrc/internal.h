@@ -78,6 +78,9 @@ bool merge_launches(const Plan& P);  // whether launch_merge enqueues a kernel f
 // Streams buf (reps + 1 launches, the first not counted) and writes per-XCD weights.
 libra_status measure_xcd_weights(const void* buf, size_t bytes, int reps, int32_t* weights,
                                  hipStream_t s);
+// Streams buf with every CU reading: fixed-interval and completion-timed rates, in GB/s.
+libra_status measure_hbm_read_rate(const void* buf, size_t bytes, int reps, double* interval_gbps,
+                                   double* completion_gbps, hipStream_t s);
 hipError_t launch_chunk(const KvLayout& L, const Plan& P, void* ws, const void* q,
                         const int32_t* bt, int32_t stride, float scale, void* out, float* lse,
                         hipStream_t s);

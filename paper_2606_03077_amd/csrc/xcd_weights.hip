@@ -58,7 +58,88 @@ __global__ __launch_bounds__(kThreads) void xcd_read_kernel(const u32x4* src, si
   }
 }
 
+// Reads [src, src + n16 * 16 bytes) once: workgroup w streams its contiguous block with
+// 16-byte non-temporal loads, four in flight per lane, and folds them into one 16-byte
+// value per workgroup so that no load is dropped.
+__global__ __launch_bounds__(kThreads) void stream_read_kernel(const u32x4* src, size_t per_wg,
+                                                               u32x4* sink) {
+  const u32x4* p = src + size_t(blockIdx.x) * per_wg;
+  u32x4 acc = {0u, 0u, 0u, 0u};
+  for (size_t i = threadIdx.x; i < per_wg; i += kThreads * kUnroll) {
+    u32x4 v[kUnroll];
+#pragma unroll
+    for (int k = 0; k < kUnroll; ++k) v[k] = __builtin_nontemporal_load(p + i + k * kThreads);
+#pragma unroll
+    for (int k = 0; k < kUnroll; ++k) acc ^= v[k];
+  }
+  __shared__ u32x4 red[kThreads];
+  red[threadIdx.x] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    u32x4 r = {0u, 0u, 0u, 0u};
+    for (int t = 0; t < kThreads; ++t) r ^= red[t];
+    sink[blockIdx.x] = r;
+  }
+}
+
 }  // namespace
+
+libra_status measure_hbm_read_rate(const void* buf, size_t bytes, int reps, double* interval_gbps,
+                                   double* completion_gbps, hipStream_t s) {
+  const size_t chunk = size_t(kThreads) * kUnroll;  // 16-byte elements
+  const size_t per_wg = (bytes / 16 / kWorkgroups) / chunk * chunk;
+  void* d = nullptr;
+  hipError_t e = hipMalloc(&d, sizeof(Count) * kWorkgroups);
+  if (e != hipSuccess) return hip_error(e, "hipMalloc(read-rate counts)");
+  Count* d_counts = static_cast<Count*>(d);
+  std::vector<Count> h(kWorkgroups);
+  hipEvent_t a = nullptr, b = nullptr;
+  e = hipEventCreate(&a);
+  if (e == hipSuccess) e = hipEventCreate(&b);
+  std::vector<double> interval, completion;
+  // Completion-timed reads first: consecutive passes over a buffer larger than the
+  // 256 MB MALL find none of their lines cached (each pass starts where the previous
+  // one's surviving lines are not).  Then the fixed-interval reads.
+  for (int r = 0; e == hipSuccess && r <= reps; ++r) {  // round 0 warms up, not counted
+    e = hipEventRecord(a, s);
+    if (e == hipSuccess) {
+      hipLaunchKernelGGL(stream_read_kernel, dim3(kWorkgroups), dim3(kThreads), 0, s,
+                         static_cast<const u32x4*>(buf), per_wg, static_cast<u32x4*>(d));
+      e = hipGetLastError();
+    }
+    if (e == hipSuccess) e = hipEventRecord(b, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    float ms = 0.f;
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, a, b);
+    if (e == hipSuccess && r > 0)
+      completion.push_back(double(per_wg) * kWorkgroups * 16.0 / (double(ms) * 1e-3) / 1e9);
+  }
+  for (int r = 0; e == hipSuccess && r <= reps; ++r) {
+    hipLaunchKernelGGL(xcd_read_kernel, dim3(kWorkgroups), dim3(kThreads), 0, s,
+                       static_cast<const u32x4*>(buf), per_wg, d_counts);
+    e = hipGetLastError();
+    if (e == hipSuccess)
+      e = hipMemcpyAsync(h.data(), d_counts, sizeof(Count) * kWorkgroups, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess || r == 0) continue;
+    // every workgroup read for kTicks of the 100 MHz clock; its first lane's load count
+    // stands for each of its lanes, 16 bytes a load
+    double loads = 0;
+    for (const Count& c : h) loads += double(c.loads);
+    interval.push_back(loads * kThreads * 16.0 / (double(kTicks) * 1e-8) / 1e9);
+  }
+  if (a) (void)hipEventDestroy(a);
+  if (b) (void)hipEventDestroy(b);
+  (void)hipFree(d);
+  if (e != hipSuccess) return hip_error(e, "HBM read-rate measurement");
+  auto median = [](std::vector<double> v) {
+    std::sort(v.begin(), v.end());
+    return v.size() % 2 ? v[v.size() / 2] : 0.5 * (v[v.size() / 2 - 1] + v[v.size() / 2]);
+  };
+  *interval_gbps = median(interval);
+  *completion_gbps = median(completion);
+  return LIBRA_OK;
+}
 
 libra_status measure_xcd_weights(const void* buf, size_t bytes, int reps, int32_t* weights,
                                  hipStream_t s) {

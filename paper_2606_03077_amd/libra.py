@@ -31,7 +31,7 @@ UNIT_FIELDS = ("b", "g", "kv_begin", "kv_end", "q_begin", "q_end", "split", "n_s
 EXPORTS = ("libra_status_string", "libra_last_error", "libra_kv_layout_create",
            "libra_kv_layout_destroy", "libra_kv_pack_pages", "libra_kv_unpack_pages",
            "libra_kv_gather", "libra_kv_copy_out", "libra_kv_copy_in", "libra_kv_reshard_host",
-           "libra_xcd_read_weights", "libra_splitkv_plan", "libra_plan_get_units",
+           "libra_xcd_read_weights", "libra_hbm_read_rate", "libra_splitkv_plan", "libra_plan_get_units",
            "libra_plan_get_info",
            "libra_plan_workspace_bytes", "libra_plan_upload", "libra_plan_destroy",
            "libra_decode_attn", "libra_decode_attn_noalloc", "libra_append_attn",
@@ -126,6 +126,7 @@ def load() -> ctypes.CDLL:
         "libra_splitkv_plan": (ctypes.c_int, [ctypes.POINTER(PlanDesc), I32P, I32P,
                                               ctypes.POINTER(PlanParams), ctypes.POINTER(P)]),
         "libra_xcd_read_weights": (ctypes.c_int, [P, SZ, I32, I32P, P]),
+        "libra_hbm_read_rate": (ctypes.c_int, [P, SZ, I32, DP, DP, P]),
         "libra_plan_get_units": (ctypes.c_int, [P, ctypes.POINTER(I32P), I32P]),
         "libra_plan_get_info": (ctypes.c_int, [P, ctypes.POINTER(PlanInfo)]),
         "libra_plan_workspace_bytes": (SZ, [P]),
@@ -316,6 +317,16 @@ def libra_xcd_read_weights(buf, reps: int = 5, stream=None) -> list:
     _check(load().libra_xcd_read_weights(_ptr(buf), nbytes, reps, w, _stream(stream)),
            "libra_xcd_read_weights")
     return list(w)
+
+
+def libra_hbm_read_rate(buf, reps: int = 5, stream=None) -> tuple:
+    """(fixed-interval GB/s, completion-timed GB/s) of streaming the device buffer `buf`
+    (>= 1 GiB) with every CU reading."""
+    iv, cp = ctypes.c_double(), ctypes.c_double()
+    nbytes = buf.numel() * buf.element_size()
+    _check(load().libra_hbm_read_rate(_ptr(buf), nbytes, reps, ctypes.byref(iv), ctypes.byref(cp),
+                                      _stream(stream)), "libra_hbm_read_rate")
+    return iv.value, cp.value
 
 
 def libra_plan_get_units(plan: int) -> np.ndarray:

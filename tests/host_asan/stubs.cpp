@@ -21,6 +21,7 @@ hipError_t launch_merge(const Plan&, void*, void*, float*, hipStream_t) { return
 bool merge_launches(const Plan&) { return false; }
 hipError_t launch_chunk(const KvLayout&, const Plan&, void*, const void*, const int32_t*, int32_t, float, void*, float*, hipStream_t) { return LAUNCH_RESULT; }
 libra_status measure_xcd_weights(const void*, size_t, int, int32_t*, hipStream_t) { return LIBRA_E_HIP; }
+libra_status measure_hbm_read_rate(const void*, size_t, int, double*, double*, hipStream_t) { return LIBRA_E_HIP; }
 hipError_t launch_page_copy(const KvLayout&, const int32_t*, int64_t, void*, void*, bool, hipStream_t) { return LAUNCH_RESULT; }
 // The static device scratch lives in device code; here it is a host array.
 size_t scratch_capacity() { return size_t(8) << 20; }

@@ -179,6 +179,21 @@ def test_xcd_read_weights_validation_codes():
     assert call(fake, 1024 * mib, 101) == 1               # reps > 100
 
 
+def test_hbm_read_rate_validation_codes():
+    # Argument checks come before any HIP call (fake device addresses are never touched).
+    lib = libra.load()
+    a, b = ctypes.c_double(), ctypes.c_double()
+    fake, mib = 1 << 30, 1 << 20
+    call = lambda buf, nbytes, reps, x=ctypes.byref(a), y=ctypes.byref(b): \
+        lib.libra_hbm_read_rate(buf, nbytes, reps, x, y, None)
+    assert call(None, 1024 * mib, 1) == 1                 # NULL buffer
+    assert call(fake, 1024 * mib, 1, None) == 1           # NULL output
+    assert call(fake, 1024 * mib, 1, ctypes.byref(a), None) == 1
+    assert call(fake + 16, 1024 * mib, 1) == 1            # not 256-byte aligned
+    assert call(fake, 1024 * mib - 1, 1) == 1             # smaller than 1 GiB
+    assert call(fake, 1024 * mib, 0) == 1 and call(fake, 1024 * mib, 101) == 1
+
+
 def test_layout_validation_codes():
     lib = libra.load()
     fake = 1 << 20

@@ -27,6 +27,17 @@ def test_xcd_read_weights_are_sane():
     assert max(w) == 1000
 
 
+def test_hbm_read_rate_is_sane():
+    """Both read rates are positive, below the 8 TB/s peak plus slack, and the
+    fixed-interval rate (no ramp or tail) is not below the completion-timed one by much."""
+    buf = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    H.say("[case] HBM read rate, 1 GiB")
+    interval, completion = libra.libra_hbm_read_rate(buf, reps=3)
+    H.say(f"[hbm] interval {interval:.0f} GB/s, completion {completion:.0f} GB/s")
+    assert 1000 < completion < 9000 and 1000 < interval < 9000
+    assert interval > 0.8 * completion
+
+
 @pytest.mark.parametrize("weights", [None, (1000, 1, 1000, 1, 1000, 1, 1000, 1),
                                      (1, 10, 100, 1000, 1000000, 7, 0, 910), "measured"])
 def test_weighted_one_wave_decode_matches_oracle(weights):
