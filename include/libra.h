@@ -292,12 +292,14 @@ libra_status libra_xcd_read_weights(const void* buf, size_t bytes, int32_t reps,
                                     int32_t* weights, void* stream);
 /* Measures the device's achievable HBM read rate, the ceiling a bandwidth-bound kernel is
  * compared with beside the vendor's peak.  `buf` (device memory of any contents, 256-byte
- * aligned, bytes >= 1 GiB, only read) is cut into 2048 contiguous blocks, one per
+ * aligned, bytes >= 256 MiB, only read) is cut into 2048 contiguous blocks, one per
  * workgroup of 256 threads (8 per CU on 256 CUs), each streamed with 16-byte non-temporal
  * loads, four in flight per lane.  completion_gbps: one pass over the whole buffer timed
  * by events around the launch (ramp and tail included, as for any kernel that must finish
  * its bytes); interval_gbps: the loads issued while every workgroup reads for 100 us of
- * the device's constant clock.  Each is the median of `reps` runs (1 <= reps <= 100)
+ * the device's constant clock (each workgroup re-reads the start of its block, so this
+ * figure needs a buffer several times the 256 MB last-level cache, whose hits would
+ * inflate it).  Each is the median of `reps` runs (1 <= reps <= 100)
  * after one warm-up run.  Allocates 64 KiB of device memory for the call and waits for
  * `stream`: for set-up and measurement, not for graph capture. */
 libra_status libra_hbm_read_rate(const void* buf, size_t bytes, int32_t reps,

@@ -593,7 +593,7 @@ libra_status libra_hbm_read_rate(const void* buf, size_t bytes, int32_t reps,
     return set_error(LIBRA_E_INVAL, "buf or an output is NULL");
   if (reinterpret_cast<uintptr_t>(buf) % kWorkspaceAlign)
     return set_error(LIBRA_E_INVAL, "buf must be 256-byte aligned");
-  if (bytes < (size_t(1) << 30)) return set_error(LIBRA_E_INVAL, "buf must hold at least 1 GiB");
+  if (bytes < (size_t(1) << 28)) return set_error(LIBRA_E_INVAL, "buf must hold at least 256 MiB");
   if (reps < 1 || reps > 100) return set_error(LIBRA_E_INVAL, "reps must lie in [1, 100]");
   return measure_hbm_read_rate(buf, bytes, reps, interval_gbps, completion_gbps,
                                static_cast<hipStream_t>(stream));

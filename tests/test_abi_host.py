@@ -190,7 +190,7 @@ def test_hbm_read_rate_validation_codes():
     assert call(fake, 1024 * mib, 1, None) == 1           # NULL output
     assert call(fake, 1024 * mib, 1, ctypes.byref(a), None) == 1
     assert call(fake + 16, 1024 * mib, 1) == 1            # not 256-byte aligned
-    assert call(fake, 1024 * mib - 1, 1) == 1             # smaller than 1 GiB
+    assert call(fake, 256 * mib - 1, 1) == 1              # smaller than 256 MiB
     assert call(fake, 1024 * mib, 0) == 1 and call(fake, 1024 * mib, 101) == 1
 
 
