@@ -79,6 +79,13 @@ typedef struct libra_plan_s* libra_plan;
 const char* libra_status_string(libra_status status);
 /* Detail of the last error raised on the calling thread ("" if none). */
 const char* libra_last_error(void);
+/* Number of HIP calls this library has made, process-wide, that allocate or free device
+ * or pinned host memory or create an event or a stream (hipMalloc, hipHostMalloc,
+ * hipFree, hipEventCreate*, hipStreamCreate*).  Plan creation may make such calls (its
+ * pinned staging image and events come from a pool that grows to the number of live
+ * plans); decode and append calls with per-kernel timing off make none, which a caller
+ * (or a test) can check by reading the count before and after. */
+uint64_t libra_alloc_calls(void);
 
 /* ------------------------------------------------------------------------------ */
 /* Paged KV cache layout                                                           */

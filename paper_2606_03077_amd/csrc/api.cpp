@@ -29,6 +29,12 @@ libra_status hip_error(hipError_t e, const char* what) {
 }
 
 namespace {
+std::atomic<uint64_t> g_alloc_calls{0};
+}
+
+void note_alloc_call() { g_alloc_calls.fetch_add(1, std::memory_order_relaxed); }
+
+namespace {
 
 constexpr size_t kWorkspaceAlign = 256;
 
@@ -47,6 +53,7 @@ struct Profiler {
       return e;
     }
     hipEvent_t e = nullptr;
+    note_alloc_call();
     if (hipEventCreate(&e) != hipSuccess) return nullptr;
     return e;
   }
@@ -155,6 +162,7 @@ libra_status staging_acquire(Plan& P) {
     } else {
       size_t cap = 4096;
       while (cap < P.upload_bytes) cap *= 2;
+      note_alloc_call();
       hipError_t e = hipHostMalloc(&P.pinned, cap, hipHostMallocDefault);
       if (e != hipSuccess) {
         P.pinned = nullptr;
@@ -169,6 +177,7 @@ libra_status staging_acquire(Plan& P) {
       g_staging.events.pop_back();
       return LIBRA_OK;
     }
+    note_alloc_call();
     hipError_t e = hipEventCreateWithFlags(ev, hipEventDisableTiming);
     if (e != hipSuccess) {
       *ev = nullptr;
@@ -209,6 +218,7 @@ libra_status ensure_aux_stream() {
   if (dev < 0 || dev >= kMaxAuxDevices) return LIBRA_OK;  // such devices run sequentially
   std::lock_guard<std::mutex> lk(g_aux_mu);
   if (!g_aux_stream[dev]) {
+    note_alloc_call();
     e = hipStreamCreateWithFlags(&g_aux_stream[dev], hipStreamNonBlocking);
     if (e != hipSuccess) {
       g_aux_stream[dev] = nullptr;
@@ -428,6 +438,8 @@ const char* libra_status_string(libra_status s) {
 }
 
 const char* libra_last_error(void) { return g_last_error.c_str(); }
+
+uint64_t libra_alloc_calls(void) { return g_alloc_calls.load(std::memory_order_relaxed); }
 
 libra_status libra_kv_layout_create(const libra_kv_layout_desc* desc, libra_kv_layout* out) {
   if (!out) return set_error(LIBRA_E_INVAL, "out is NULL");

@@ -50,6 +50,10 @@ struct KvLayout {
   libra_kv_layout_desc desc{};
 };
 
+// Counts every HIP call of the library that allocates or frees memory or creates an
+// event or a stream (libra_alloc_calls reports the total).
+void note_alloc_call();
+
 // Error reporting (per thread).
 libra_status set_error(libra_status s, const std::string& msg);
 libra_status hip_error(hipError_t e, const char* what);

@@ -89,11 +89,14 @@ libra_status measure_hbm_read_rate(const void* buf, size_t bytes, int reps, doub
   const size_t chunk = size_t(kThreads) * kUnroll;  // 16-byte elements
   const size_t per_wg = (bytes / 16 / kWorkgroups) / chunk * chunk;
   void* d = nullptr;
+  note_alloc_call();
   hipError_t e = hipMalloc(&d, sizeof(Count) * kWorkgroups);
   if (e != hipSuccess) return hip_error(e, "hipMalloc(read-rate counts)");
   Count* d_counts = static_cast<Count*>(d);
   std::vector<Count> h(kWorkgroups);
   hipEvent_t a = nullptr, b = nullptr;
+  note_alloc_call();
+  note_alloc_call();
   e = hipEventCreate(&a);
   if (e == hipSuccess) e = hipEventCreate(&b);
   std::vector<double> interval, completion;
@@ -130,6 +133,7 @@ libra_status measure_hbm_read_rate(const void* buf, size_t bytes, int reps, doub
   }
   if (a) (void)hipEventDestroy(a);
   if (b) (void)hipEventDestroy(b);
+  note_alloc_call();
   (void)hipFree(d);
   if (e != hipSuccess) return hip_error(e, "HBM read-rate measurement");
   auto median = [](std::vector<double> v) {
@@ -146,6 +150,7 @@ libra_status measure_xcd_weights(const void* buf, size_t bytes, int reps, int32_
   const size_t chunk = size_t(kThreads) * kUnroll;  // 16-byte elements
   const size_t per_wg = (bytes / 16 / kWorkgroups) / chunk * chunk;
   Count* d_counts = nullptr;
+  note_alloc_call();
   hipError_t e = hipMalloc(&d_counts, sizeof(Count) * kWorkgroups);
   if (e != hipSuccess) return hip_error(e, "hipMalloc(counts)");
   std::vector<Count> h(kWorkgroups);
@@ -165,6 +170,7 @@ libra_status measure_xcd_weights(const void* buf, size_t bytes, int reps, int32_
     if (r == 0) continue;
     for (const Count& c : h) loads[c.xcc % kNumXcds] += double(c.loads);
   }
+  note_alloc_call();
   (void)hipFree(d_counts);
   if (st != LIBRA_OK) return st;
   double most = 0;

@@ -28,7 +28,8 @@ UNIT_INTS = 12
 UNIT_FIELDS = ("b", "g", "kv_begin", "kv_end", "q_begin", "q_end", "split", "n_splits",
                "part_base", "row0", "kind", "prior")
 
-EXPORTS = ("libra_status_string", "libra_last_error", "libra_kv_layout_create",
+EXPORTS = ("libra_status_string", "libra_last_error", "libra_alloc_calls",
+           "libra_kv_layout_create",
            "libra_kv_layout_destroy", "libra_kv_pack_pages", "libra_kv_unpack_pages",
            "libra_kv_gather", "libra_kv_copy_out", "libra_kv_copy_in", "libra_kv_reshard_host",
            "libra_xcd_read_weights", "libra_hbm_read_rate", "libra_splitkv_plan", "libra_plan_get_units",
@@ -114,6 +115,7 @@ def load() -> ctypes.CDLL:
     sig = {
         "libra_status_string": (ctypes.c_char_p, [ctypes.c_int]),
         "libra_last_error": (ctypes.c_char_p, []),
+        "libra_alloc_calls": (ctypes.c_uint64, []),
         "libra_kv_layout_create": (ctypes.c_int, [ctypes.POINTER(LayoutDesc), ctypes.POINTER(P)]),
         "libra_kv_layout_destroy": (None, [P]),
         "libra_kv_pack_pages": (ctypes.c_int, [P, P, P, I64, I64, P]),
@@ -228,6 +230,11 @@ def libra_status_string(status: int) -> str:
 
 def libra_last_error() -> str:
     return load().libra_last_error().decode()
+
+
+def libra_alloc_calls() -> int:
+    """HIP allocate / free / event / stream creation calls the library has made so far."""
+    return int(load().libra_alloc_calls())
 
 
 def libra_kv_layout_create(k_cache, v_cache, num_pages: int, num_kv_heads: int,

@@ -328,3 +328,14 @@ def test_traffic_keys_follow_the_unit_set():
                                          num_cus=256)
             assert entry["plan_sha"] == bench.plan_sha(libra.libra_plan_get_units(h)), (kernel, name)
             libra.libra_plan_destroy(h)
+
+
+def test_alloc_call_count_is_exported_and_host_planning_allocates_nothing():
+    """Without a visible device a plan takes no pinned image or events, so building and
+    destroying one makes no HIP allocation call (the GPU tests check decode / append)."""
+    before = libra.libra_alloc_calls()
+    assert before >= 0
+    h = libra.libra_splitkv_plan(libra.LIBRA_MODE_APPEND, 3, 32, 8, [700, 300, 64], [1, 200, 64],
+                                 num_cus=16)
+    libra.libra_plan_destroy(h)
+    assert libra.libra_alloc_calls() == before
