@@ -1,9 +1,9 @@
 // Decode attention over the paged KV cache, one 256-thread workgroup per plan unit.
 //
 // A unit is (sequence b, KV head g, KV range [kv0, kv1)).  Its pages are shared out to
-// the 4 wavefronts in contiguous quarters.  For each page a wave issues eight 16-byte
-// loads per lane (K and V; the layout makes each a contiguous 1 KiB wave-wide read) one
-// page ahead of the math, then on the matrix cores:
+// the 4 wavefronts in contiguous quarters.  For each page a wave issues four 16-byte K
+// loads and eight 8-byte V loads per lane (the layout makes each a contiguous 1 KiB or
+// 512 B wave-wide read) one page ahead of the math, then on the matrix cores:
 //
 //   S^T[16 slots x 16 heads] = K[16 x 128] . Q^T[128 x 16]    (4 x mfma 16x16x32)
 //   O^T[128 x 16 heads]     += V^T[128 x 16 slots] . P^T[16 x 16]  (8 x mfma 16x16x16)
@@ -46,7 +46,7 @@ constexpr float kLn2 = 0.6931471805599453f;
 
 struct PageRegs {
   uint4 k[4];  // K tile, 16 B per lane per 1 KiB quarter
-  uint4 v[4];  // V tile, same
+  uint2 v[8];  // V: this lane's 4 slots of one channel for each 16-channel block
 };
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 x) { return __builtin_bit_cast(bf16x8, x); }
@@ -60,11 +60,22 @@ __device__ __forceinline__ uint4 stream_load(const uint4* p) {
   return make_uint4(v.x, v.y, v.z, v.w);
 }
 
-__device__ __forceinline__ void load_page(PageRegs& r, const uint4* kt, const uint4* vt, int lane) {
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint2 stream_load2(const uint2* p) {
+  const u32x2 v = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(p));
+  return make_uint2(v.x, v.y);
+}
+
+// V of lane (i, quad) for channel block db: slots 4 quad .. + 3 of channel 16 db + i, the
+// half quad / 2 of granule 2 (16 db + i) + quad % 2 (8 bytes; a wave reads 512 contiguous
+// bytes per block).
+__device__ __forceinline__ void load_page(PageRegs& r, const uint4* kt, const uint2* vt, int lane) {
 #pragma unroll
   for (int i = 0; i < 4; ++i) r.k[i] = stream_load(kt + i * 64 + lane);
+  const int col = lane & 15, quad = lane >> 4;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) r.v[i] = stream_load(vt + i * 64 + lane);
+  for (int db = 0; db < 8; ++db)
+    r.v[db] = stream_load2(vt + 2 * (2 * (16 * db + col) + (quad & 1)) + (quad >> 1));
 }
 
 // Zero V of slots >= valid (slot = 4 * quad + r): keeps NaN/garbage of unused slots
@@ -76,11 +87,9 @@ __device__ __forceinline__ void clear_v_slots(PageRegs& r, int quad, int valid) 
   const uint32_t m0 = keep >= 2 ? 0xFFFFFFFFu : (keep == 1 ? 0x0000FFFFu : 0u);
   const uint32_t m1 = keep >= 4 ? 0xFFFFFFFFu : (keep == 3 ? 0x0000FFFFu : 0u);
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+  for (int i = 0; i < 8; ++i) {
     r.v[i].x &= m0;
     r.v[i].y &= m1;
-    r.v[i].z &= m0;
-    r.v[i].w &= m1;
   }
 }
 
@@ -136,8 +145,7 @@ __device__ __forceinline__ void process_page(const PageRegs& r, int valid, int q
   const bf16x4_bits pop = as_bf16x4(pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]));
 #pragma unroll
   for (int db = 0; db < 8; ++db) {
-    const uint4 v = r.v[db >> 1];
-    const bf16x4_bits vop = (db & 1) ? as_bf16x4(v.z, v.w) : as_bf16x4(v.x, v.y);
+    const bf16x4_bits vop = as_bf16x4(r.v[db].x, r.v[db].y);
     acc[db] *= alpha;
     acc[db] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vop, pop, acc[db], 0, 0, 0);
   }
@@ -216,7 +224,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(LIBRA_
       const int64_t page = __builtin_amdgcn_readlane(ids_cur, k - win);
       const size_t base = size_t(page) * page_stride + head_off;
       load_page(r, reinterpret_cast<const uint4*>(A.k_cache + base),
-                reinterpret_cast<const uint4*>(A.v_cache + base), lane);
+                reinterpret_cast<const uint2*>(A.v_cache + base), lane);
     };
     auto consume = [&](PageRegs& r, int k) {
       const int valid = min(kPage, kv1 - (w0 + k) * kPage);
