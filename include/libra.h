@@ -99,12 +99,12 @@ uint64_t libra_alloc_calls(void);
  * (slot s, channel d) sits at:
  *
  *   K: ((d / 8) * 16 + s) * 8 + d % 8
- *   V: (2 * d + (s / 4) % 2) * 8 + (s / 8) * 4 + s % 4
+ *   V: (128 * ((s / 4) % 2) + d) * 8 + (s / 8) * 4 + s % 4
  *
  * i.e. the order in which a 64-lane wavefront consumes them as matrix-core operands:
- * a K granule (16 bytes) is one slot's 8 consecutive channels; V granule 2 d + h holds
- * channel d's slots {4h..4h+3, 8+4h..11+4h}, the 8 keys one lane of a 32x32x16 product
- * takes, so one 16-byte load per lane reads 1 KiB contiguously.  Callers never address
+ * a K granule (16 bytes) is one slot's 8 consecutive channels; V granule 128 h + d
+ * holds channel d's slots {4h..4h+3, 8+4h..11+4h}, the 8 keys one lane of a 32x32x16
+ * product takes, so one 16-byte load per lane reads 1 KiB contiguously.  Callers never address
  * elements directly: libra_kv_pack_pages / libra_kv_unpack_pages convert whole pages
  * from / to the logical format, and libra_append_attn writes new tokens.
  *

@@ -16,8 +16,9 @@
 //   O^T[128 channels x 32 rows] += V^T . P^T: per page, 4 MFMAs (32-channel blocks) over
 //     the page's 16 keys.  A lane's probabilities of one page, keys {4h..4h+3, 8+4h..
 //     11+4h} in that order, are its B operand as they come out of the scores; the
-//     matching A operand, channel d's values at those keys, is V granule 2 d + h of the
-//     stored tile (one 16-byte LDS read), which is why V tiles are stored in that order.
+//     matching A operand, channel d's values at those keys, is V granule 128 h + d of
+//     the stored tile (one 16-byte LDS read; the 32 lanes of one half read 512 contiguous
+//     bytes, free of bank conflicts), which is why V tiles are stored in that order.
 // Each wave works through a step by page pairs: the pair's K operands for step n + 1
 // are read from LDS first, then the pair's probabilities are formed (exps) while they
 // land, then step n + 1's scores of the pair (a dependent chain of 8 MFMAs) are issued
@@ -259,7 +260,7 @@ void chunk_kernel(ChunkArgs A) {
   // Page pair P of step n: probabilities (consuming s[P]), step n + 1's scores of the
   // pair (from stage kread, unless last) and O^T += V^T P^T over the pair's two pages
   // from V stage vread.  V operand of page j, channel block cb: lane (channel
-  // 32 cb + col, hh) reads granule 2 (32 cb + col) + hh, keys in the order of the P
+  // 32 cb + col, hh) reads granule 128 hh + 32 cb + col, keys in the order of the P
   // operand (element p: slot 8 (p / 4) + 4 hh + p % 4), which is the score layout.
   auto pair = [&](int P, auto kread, auto vread, int key0, f32x16 (&s)[2], float neg_m,
                   auto last_tag) {
@@ -312,7 +313,7 @@ void chunk_kernel(ChunkArgs A) {
         qs = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kpre[c]), qop[c], qs, 0, 0, 0);
       }
       const int jj = c >> 2, cb = c & 3;
-      uint4 vo = vst(vread)[2 * P + jj][2 * (32 * cb + col) + hh];
+      uint4 vo = vst(vread)[2 * P + jj][128 * hh + 32 * cb + col];
       if constexpr (kLast) {
         vo.x &= mk[jj][0];
         vo.y &= mk[jj][1];

@@ -2,8 +2,9 @@
 //
 // A unit is (sequence b, KV head g, KV range [kv0, kv1)).  Its pages are shared out to
 // the 4 wavefronts in contiguous quarters.  For each page a wave issues four 16-byte K
-// loads and eight 8-byte V loads per lane (the layout makes each a contiguous 1 KiB or
-// 512 B wave-wide read) one page ahead of the math, then on the matrix cores:
+// loads and eight 8-byte V loads per lane (the layout makes each K load one contiguous
+// 1 KiB wave-wide read, each V load two 256 B runs) one page ahead of the math, then on
+// the matrix cores:
 //
 //   S^T[16 slots x 16 heads] = K[16 x 128] . Q^T[128 x 16]    (4 x mfma 16x16x32)
 //   O^T[128 x 16 heads]     += V^T[128 x 16 slots] . P^T[16 x 16]  (8 x mfma 16x16x16)
@@ -67,15 +68,15 @@ __device__ __forceinline__ uint2 stream_load2(const uint2* p) {
 }
 
 // V of lane (i, quad) for channel block db: slots 4 quad .. + 3 of channel 16 db + i, the
-// half quad / 2 of granule 2 (16 db + i) + quad % 2 (8 bytes; a wave reads 512 contiguous
-// bytes per block).
+// half quad / 2 of granule 128 (quad % 2) + 16 db + i (8 bytes; a wave reads two runs of
+// 256 contiguous bytes per block).
 __device__ __forceinline__ void load_page(PageRegs& r, const uint4* kt, const uint2* vt, int lane) {
 #pragma unroll
   for (int i = 0; i < 4; ++i) r.k[i] = stream_load(kt + i * 64 + lane);
   const int col = lane & 15, quad = lane >> 4;
 #pragma unroll
   for (int db = 0; db < 8; ++db)
-    r.v[db] = stream_load2(vt + 2 * (2 * (16 * db + col) + (quad & 1)) + (quad >> 1));
+    r.v[db] = stream_load2(vt + 2 * (128 * (quad & 1) + 16 * db + col) + (quad >> 1));
 }
 
 // Zero V of slots >= valid (slot = 4 * quad + r): keeps NaN/garbage of unused slots

@@ -19,9 +19,9 @@ constexpr int kThreads = 256;
 __device__ __forceinline__ int k_off(int s, int d) { return ((d >> 3) * 16 + s) * 8 + (d & 7); }
 
 // Position of (slot s, channel d) inside a V tile, in bf16 elements: 16-byte granule
-// 2 d + h holds channel d's slots {4 h .. 4 h + 3, 8 + 4 h .. 11 + 4 h}, h = (s / 4) % 2.
+// 128 h + d holds channel d's slots {4 h .. 4 h + 3, 8 + 4 h .. 11 + 4 h}, h = (s / 4) % 2.
 __device__ __forceinline__ int v_off(int s, int d) {
-  return (2 * d + ((s >> 2) & 1)) * 8 + (s >> 3) * 4 + (s & 3);
+  return (128 * ((s >> 2) & 1) + d) * 8 + (s >> 3) * 4 + (s & 3);
 }
 
 __device__ __forceinline__ size_t tile_elem(int64_t page, int g, int hkv) {
