@@ -23,10 +23,13 @@
 // are read from LDS first, then the pair's probabilities are formed (exps) while they
 // land, then step n + 1's scores of the pair (a dependent chain of 8 MFMAs) are issued
 // interleaved with the pair's 8 independent PV products.
-// Softmax runs online in base 2.  The running maximum is only moved (and the
-// accumulators rescaled) when a step's scores exceed it by more than 2^kTau, which a
-// wave-wide vote detects; otherwise probabilities are taken against the old maximum
-// (at most 2^kTau, exact in the final normalisation).  Causal masks are applied only on
+// Softmax runs online in base 2 against a running maximum that is set exactly on the
+// first step and afterwards moved only when needed: the probabilities of a page pair
+// are taken against the current maximum, and if any lane's sum of them exceeds 2^kTau
+// (which any probability above 2^kTau forces), a wave-wide vote moves the maximum to
+// the pair's own, rescales the accumulators and takes them again, before a product uses
+// them.  Probabilities therefore stay at most 2^kTau, and the result is exact after the
+// final normalisation; no per-step maximum is taken.  Causal masks are applied only on
 // steps that reach past the tile's first token.  Row r = 32 w + column of the tile is
 // token q0 + r / G, head r % G; it sees keys k <= P_b + token.
 // Units arrive in per-XCD queues: workgroup w takes tile w / 8 of queue w % 8, so the
@@ -49,6 +52,7 @@ constexpr int kThreads = 64 * kWaves;
 static_assert(kChunkRows == 32 * kWaves, "the plan's tile rows are the kernel's");
 constexpr int kStepPages = 4;    // pages (16 keys each) per softmax step
 constexpr float kTau = 8.f;       // lazy-rescale threshold, base-2 logits
+constexpr float kSumTau = 256.f;  // 2^kTau
 constexpr int kMaxIds = 4096;     // block-table entries staged in LDS (64K keys)
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
@@ -231,7 +235,9 @@ void chunk_kernel(ChunkArgs A) {
   };
 
   // Causal / length mask and running-maximum update for step n.
-  auto prepare = [&](int key0, f32x16 (&s)[2], float& neg_m) {
+  // Causal / length mask of step n; on the first step (exact) also the running maximum
+  // (later steps check their probabilities instead, in pair()).
+  auto prepare = [&](int key0, f32x16 (&s)[2], float& neg_m, bool exact) {
     if (key0 > mask_key0) {
 #pragma unroll
       for (int P = 0; P < 2; ++P)
@@ -239,21 +245,30 @@ void chunk_kernel(ChunkArgs A) {
         for (int r = 0; r < 16; ++r)
           if (key0 + 32 * P + acc_row(r, hh) > lim) s[P][r] = -INFINITY;
     }
+    if (exact) {
+      float mloc = -INFINITY;
+#pragma unroll
+      for (int P = 0; P < 2; ++P)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mloc = fmaxf(mloc, s[P][r]);
+      float mc = fmaxf(mloc * A.sl2, m);
+      m = fmaxf(mc, __shfl_xor(mc, 32));
+    }
+    neg_m = m == -INFINITY ? 0.f : -m;
+  };
+  // Moves the running maximum to cover page pair P's scores (rare): rescales l and the
+  // accumulators by 2^(m_old - m_new).
+  auto rescale = [&](const f32x16& sp, float& neg_m) {
     float mloc = -INFINITY;
 #pragma unroll
-    for (int P = 0; P < 2; ++P)
+    for (int r = 0; r < 16; ++r) mloc = fmaxf(mloc, sp[r]);
+    float mc = fmaxf(mloc * A.sl2, m);
+    mc = fmaxf(mc, __shfl_xor(mc, 32));
+    const float alpha = m == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m - mc);
+    l *= alpha;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) mloc = fmaxf(mloc, s[P][r]);
-    const float xmax = mloc * A.sl2;
-    if (__ballot(xmax > m + kTau)) {
-      float mc = fmaxf(xmax, m);
-      mc = fmaxf(mc, __shfl_xor(mc, 32));
-      const float alpha = m == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m - mc);
-      l *= alpha;
-#pragma unroll
-      for (int cb = 0; cb < 4; ++cb) acc[cb] *= alpha;
-      m = mc;
-    }
+    for (int cb = 0; cb < 4; ++cb) acc[cb] *= alpha;
+    m = mc;
     neg_m = m == -INFINITY ? 0.f : -m;
   };
 
@@ -262,7 +277,7 @@ void chunk_kernel(ChunkArgs A) {
   // from V stage vread.  V operand of page j, channel block cb: lane (channel
   // 32 cb + col, hh) reads granule 128 hh + 32 cb + col, keys in the order of the P
   // operand (element p: slot 8 (p / 4) + 4 hh + p % 4), which is the score layout.
-  auto pair = [&](int P, auto kread, auto vread, int key0, f32x16 (&s)[2], float neg_m,
+  auto pair = [&](int P, auto kread, auto vread, int key0, f32x16 (&s)[2], float& neg_m,
                   auto last_tag) {
     constexpr bool kLast = decltype(last_tag)::value;
     uint4 kpre[8];
@@ -270,12 +285,24 @@ void chunk_kernel(ChunkArgs A) {
 #pragma unroll
       for (int c = 0; c < 8; ++c) kpre[c] = kst(kread)[2 * P + (col >> 4)][(2 * c + hh) * 16 + (col & 15)];
     }
-    float p[16];
+    // Probabilities against the current maximum.  A probability above 2^kTau (the
+    // maximum is stale by more than kTau, or this is a new row's first real score)
+    // makes this lane's sum of the pair exceed 2^kTau: the wave then moves the maximum
+    // to the pair's own and takes them again, before any product has used them.
+    float p[16], ps;
+    auto take = [&]() {
 #pragma unroll
-    for (int r = 0; r < 16; ++r) p[r] = __builtin_amdgcn_exp2f(fmaf(s[P][r], A.sl2, neg_m));
-    float t0 = (p[0] + p[1]) + (p[2] + p[3]), t1 = (p[4] + p[5]) + (p[6] + p[7]);
-    float t2 = (p[8] + p[9]) + (p[10] + p[11]), t3 = (p[12] + p[13]) + (p[14] + p[15]);
-    l += (t0 + t1) + (t2 + t3);
+      for (int r = 0; r < 16; ++r) p[r] = __builtin_amdgcn_exp2f(fmaf(s[P][r], A.sl2, neg_m));
+      const float t0 = (p[0] + p[1]) + (p[2] + p[3]), t1 = (p[4] + p[5]) + (p[6] + p[7]);
+      const float t2 = (p[8] + p[9]) + (p[10] + p[11]), t3 = (p[12] + p[13]) + (p[14] + p[15]);
+      ps = (t0 + t1) + (t2 + t3);
+    };
+    take();
+    if (__ballot(!(ps <= kSumTau))) {
+      rescale(s[P], neg_m);
+      take();
+    }
+    l += ps;
     uint4 pa, pb;
     pa.x = pack_bf16x2(p[0], p[1]);
     pa.y = pack_bf16x2(p[2], p[3]);
@@ -348,7 +375,7 @@ void chunk_kernel(ChunkArgs A) {
     const int key0 = n * kStepPages * kPage;
     copy_kv(min(n + 3, nsteps - 1), Copy{});
     float neg_m;
-    prepare(key0, sc, neg_m);
+    prepare(key0, sc, neg_m, n == 0);
     pair(0, KRead{}, VRead{}, key0, sc, neg_m, std::false_type{});
     pair(1, KRead{}, VRead{}, key0, sc, neg_m, std::false_type{});
     __builtin_amdgcn_s_waitcnt(0xF74);
@@ -371,7 +398,7 @@ void chunk_kernel(ChunkArgs A) {
   if (nsteps > 0) {
     const int key0 = (nsteps - 1) * kStepPages * kPage;
     float neg_m;
-    prepare(key0, sc, neg_m);
+    prepare(key0, sc, neg_m, nsteps == 1);
     switch ((nsteps - 1) & 3) {
       case 0:
         pair(0, S0{}, S0{}, key0, sc, neg_m, std::true_type{});
