@@ -122,7 +122,7 @@ void chunk_kernel(ChunkArgs A) {
   const int q0 = u[U_Q0], q1 = u[U_Q1], row0 = u[U_ROW0], prior = u[U_PRIOR];
 
   const int tid = threadIdx.x;
-  const int wave = tid >> 6, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const int col = lane & 31, hh = lane >> 5;  // accumulator column (tile row), lane half
   const int G = A.group;
 
@@ -165,45 +165,31 @@ void chunk_kernel(ChunkArgs A) {
                        size_t(lane) * 16;
   const char* v_lane = reinterpret_cast<const char*>(A.v_cache) + size_t(g) * kTileBytes +
                        size_t(lane) * 16;
-  // The step's 4 page ids (from LDS, one broadcast read; global memory past the staged
-  // row, uniform and rare).  Pages past the end re-read the last page (the id row is
-  // padded with it), so the copies stay branch-free; their keys are >= kv1, so they
-  // are masked and their V zeroed.
-  auto step_ids = [&](int step, int (&ids)[kStepPages]) {
-    const int p0 = step * kStepPages;
-    if (p0 + kStepPages <= kMaxIds) {
-      const int4 v = *reinterpret_cast<const int4*>(&lds_ids[p0]);
-      ids[0] = v.x;
-      ids[1] = v.y;
-      ids[2] = v.z;
-      ids[3] = v.w;
-    } else {
-#pragma unroll
-      for (int j = 0; j < kStepPages; ++j)
-        ids[j] = __builtin_amdgcn_readfirstlane(btrow[min(p0 + j, npages - 1)]);
-    }
-  };
   // K and V of `step` straight into LDS stage stage_tag & 3: wave w moves 1 KiB chunks
   // 2 w and 2 w + 1 of the step's four K tiles and of its four V tiles (16 B per lane at
-  // the chunk's LDS base + 16 lane, the tile as stored).  Four vector-memory operations
-  // per wave per step, in a fixed order; the waits count them.
+  // the chunk's LDS base + 16 lane, the tile as stored).  Both chunks lie in page w / 2 of
+  // the step, so a wave needs one page id: from the staged row (a broadcast LDS read), or
+  // from global memory past it (uniform and rare).  Pages past the end re-read the last
+  // page (the id row is padded with it), so the copies stay branch-free; their keys are
+  // >= kv1, so they are masked and their V zeroed.  The wave index is made scalar, so the
+  // page, the LDS targets and the byte offsets are scalar arithmetic.  Four vector-memory
+  // operations per wave per step, in a fixed order; the waits count them.
   auto copy_kv = [&](int step, auto stage_tag) {
-    int ids[kStepPages];
-    step_ids(step, ids);
+    const int j = wave >> 1;
+    const int p = step * kStepPages + j;
+    const int id = p < kMaxIds ? __builtin_amdgcn_readfirstlane(lds_ids[p])
+                               : __builtin_amdgcn_readfirstlane(btrow[min(p, npages - 1)]);
 #pragma unroll
     for (int c2 = 0; c2 < 2; ++c2) {
-      const int c = 2 * wave + c2;
-      const int j = c >> 2, i = c & 3;
-      const uint64_t off = uint64_t(uint32_t(ids[j])) * page_bytes + i * 1024;
-      const uint32_t dk = __builtin_amdgcn_readfirstlane(
-          uint32_t(reinterpret_cast<uintptr_t>(&kst(stage_tag)[j][i * 64])));
+      const int i = (2 * wave + c2) & 3;
+      const uint64_t off = uint64_t(uint32_t(id)) * page_bytes + i * 1024;
+      const uint32_t dk = uint32_t(reinterpret_cast<uintptr_t>(&kst(stage_tag)[j][i * 64]));
       const char* ksrc = k_lane + off;
       asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
                    :
                    : "s"(dk), "v"(ksrc)
                    : "memory", "m0");
-      const uint32_t dv = __builtin_amdgcn_readfirstlane(
-          uint32_t(reinterpret_cast<uintptr_t>(&vst(stage_tag)[j][i * 64])));
+      const uint32_t dv = uint32_t(reinterpret_cast<uintptr_t>(&vst(stage_tag)[j][i * 64]));
       const char* vsrc = v_lane + off;
       asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
                    :
