@@ -51,8 +51,8 @@ constexpr int kWaves = 8;
 constexpr int kThreads = 64 * kWaves;
 static_assert(kChunkRows == 32 * kWaves, "the plan's tile rows are the kernel's");
 constexpr int kStepPages = 4;    // pages (16 keys each) per softmax step
-constexpr float kTau = 8.f;       // lazy-rescale threshold, base-2 logits
-constexpr float kSumTau = 256.f;  // 2^kTau
+constexpr int kTau = 8;           // lazy-rescale threshold, base-2 logits
+constexpr float kSumTau = float(1 << kTau);  // probabilities stay at most 2^kTau
 constexpr int kMaxIds = 4096;     // block-table entries staged in LDS (64K keys)
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
