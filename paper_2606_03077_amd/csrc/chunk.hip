@@ -344,6 +344,12 @@ void chunk_kernel(ChunkArgs A) {
   if (nsteps > 2) copy_kv(2, S2{});
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
+  // Wave priority: 1 from a step's opening barrier through its first page pair, 0 for the
+  // second.  The two waves of a SIMD otherwise share issue by age, so the older one ran
+  // each step's pairs ~40% faster than its partner and then idled at the barrier while
+  // the younger finished alone; dropping the priority of a wave once it is half-way
+  // through lets a lagging partner catch up within the step.
+  __builtin_amdgcn_s_setprio(1);
 
   f32x16 sc[2];
   if (nsteps > 0) {
@@ -363,9 +369,11 @@ void chunk_kernel(ChunkArgs A) {
     float neg_m;
     prepare(key0, sc, neg_m, n == 0);
     pair(0, KRead{}, VRead{}, key0, sc, neg_m, std::false_type{});
+    __builtin_amdgcn_s_setprio(0);
     pair(1, KRead{}, VRead{}, key0, sc, neg_m, std::false_type{});
     __builtin_amdgcn_s_waitcnt(0xF74);
     __syncthreads();
+    __builtin_amdgcn_s_setprio(1);
   };
   int n0 = 0;
   for (; n0 + 4 < nsteps; n0 += 4) {
