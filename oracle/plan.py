@@ -41,13 +41,15 @@ units per CU, minimum split size in pages, maximum splits, chunk query tile).
    [0, P_b + min(kT + T, C_b)), where P_b = L_b - C_b.  Tiles are not split along KV.
 8. Every unit is repeated for each KV head g.
 9. Single units are ordered by descending KV token count, ties by ascending (b, g, j).
-   Chunk units are grouped per (b, g); a tile costs KV tokens x query tokens and a group
-   the sum of its tiles.  With F = ceil(total cost / 8), a group of cost c and m tiles is
-   cut into n = min(m, ceil(c / F)) parts: its tile i (ascending q_begin) goes to part
+   Chunk units are grouped per (b, g); a tile costs its key-loop steps,
+   ceil((kv_end - kv_begin) / 64), and a group the sum of its tiles.  With
+   F = ceil(total cost / 8), a group of cost c and m tiles is cut into
+   n = min(m, ceil(c / F)) parts: its tile i (ascending q_begin) goes to part
    floor(S_i * n / c), S_i being the cost of the group's tiles before it; empty parts are
    dropped.  Parts, by descending cost (ties ascending (b, g, part)), are dealt to 8
    queues (one per XCD), each to the queue with the least accumulated cost (ties to the
-   lowest queue).  Within a part, tiles go by descending cost, ties ascending q_begin.
+   lowest queue).  Each queue then lists its tiles by descending cost, ties ascending
+   (b, g, q_begin).
    The table lists all single units, then queue 0's tiles, queue 1's, ... queue 7's.
 10. Single rows with n_b > 1 own n_b partial-result slots per KV head, allotted in
     ascending (b, g) order: part_base(b, g) = (slots of earlier split rows) + g * n_b.
@@ -74,6 +76,7 @@ KIND_SINGLE = 0
 KIND_CHUNK = 1
 PAGE = 16
 NUM_XCDS = 8
+CHUNK_STEP_KEYS = 64   # keys per step of the chunk kernel's key loop (step 9's tile cost)
 
 
 @dataclasses.dataclass(frozen=True)
@@ -209,7 +212,7 @@ def plan_ref(seq_lens, q_lens, num_kv_heads: int, group: int, params: PlanParams
                 q1 = min(q0 + T, C[b])
                 chunks.append((b, g, 0, P + q1, q0, q1, 0, 1, -1, row0[b], KIND_CHUNK, P))
     def cost(u):
-        return (u[3] - u[2]) * (u[5] - u[4])
+        return _ceil_div(u[3] - u[2], CHUNK_STEP_KEYS)
 
     groups = {}
     for u in chunks:                      # built in ascending (b, g, q_begin)
@@ -229,7 +232,8 @@ def plan_ref(seq_lens, q_lens, num_kv_heads: int, group: int, params: PlanParams
     for k in order:
         x = min(range(NUM_XCDS), key=lambda i: (qcost[i], i))
         qcost[x] += sum(cost(u) for u in parts[k])
-        queues[x].extend(sorted(parts[k], key=lambda u: (-cost(u), u[4])))
+        queues[x].extend(parts[k])
+    queues = [sorted(q, key=lambda u: (-cost(u), u[0], u[1], u[4])) for q in queues]
     chunks = [u for q in queues for u in q]
 
     info = {"n_single": len(singles), "n_chunk": len(chunks), "n_partial_slots": slots,

@@ -51,6 +51,7 @@ constexpr int kWaves = 8;
 constexpr int kThreads = 64 * kWaves;
 static_assert(kChunkRows == 32 * kWaves, "the plan's tile rows are the kernel's");
 constexpr int kStepPages = 4;    // pages (16 keys each) per softmax step
+static_assert(kStepPages * kPage == kChunkStepKeys, "the plan's tile cost counts these steps");
 constexpr int kTau = 8;           // lazy-rescale threshold, base-2 logits
 constexpr float kSumTau = float(1 << kTau);  // probabilities stay at most 2^kTau
 constexpr int kMaxIds = 4096;     // block-table entries staged in LDS (64K keys)

@@ -206,9 +206,12 @@ libra_status build_plan(const libra_plan_desc& d, const int32_t* seq_lens, const
   // unless the group costs more than an eighth of the launch: it is then cut into
   // contiguous, cost-balanced parts so that every XCD gets work.  Parts by descending
   // cost (ties ascending (b, g, part)) are dealt to the XCD queue with the least
-  // accumulated cost (ties to the lowest queue); inside a part, tiles by descending
-  // cost, ties ascending q_begin; queues are listed one after another.
-  auto cost = [](const Unit& u) { return int64_t(u[U_KV1] - u[U_KV0]) * (u[U_Q1] - u[U_Q0]); };
+  // accumulated cost (ties to the lowest queue); each queue then lists its tiles by
+  // descending cost, ties ascending (b, g, q_begin) (longest first, so the last tiles a
+  // CU takes are short; a group's tiles, of nearly equal cost, stay close); queues are
+  // listed one after another.  A tile costs its key-loop steps: the kernel spends the
+  // same time on a step whatever the number of the tile's query tokens.
+  auto cost = [](const Unit& u) { return ceil_div(u[U_KV1] - u[U_KV0], kChunkStepKeys); };
   int64_t total_cost = 0;
   for (const Unit& u : chunks) total_cost += cost(u);
   const int64_t fair = std::max<int64_t>(1, ceil_div(total_cost, kNumXcds));
@@ -253,14 +256,17 @@ libra_status build_plan(const libra_plan_desc& d, const int32_t* seq_lens, const
     for (int y = 1; y < kNumXcds; ++y)
       if (qcost[y] < qcost[x]) x = y;
     qcost[x] += parts[k].cost;
-    std::vector<Unit> tiles(part_tiles.begin() + parts[k].first, part_tiles.begin() + parts[k].last);
-    std::sort(tiles.begin(), tiles.end(), [&](const Unit& a, const Unit& b) {
+    queues[x].insert(queues[x].end(), part_tiles.begin() + parts[k].first,
+                     part_tiles.begin() + parts[k].last);
+  }
+  for (auto& q : queues)
+    std::sort(q.begin(), q.end(), [&](const Unit& a, const Unit& b) {
       const int64_t ca = cost(a), cb = cost(b);
       if (ca != cb) return ca > cb;
+      if (a[U_B] != b[U_B]) return a[U_B] < b[U_B];
+      if (a[U_G] != b[U_G]) return a[U_G] < b[U_G];
       return a[U_Q0] < b[U_Q0];
     });
-    queues[x].insert(queues[x].end(), tiles.begin(), tiles.end());
-  }
   chunks.clear();
   int32_t xcd_map[2 * kNumXcds];
   int32_t longest = 0;

@@ -21,6 +21,7 @@ enum UnitField : int {
 constexpr int kKindSingle = 0;
 constexpr int kKindChunk = 1;
 constexpr int kNumXcds = 8;  // MI355X: workgroup w is dispatched to XCD w % 8
+constexpr int kChunkStepKeys = 64;  // keys per step of the chunk kernel's key loop
 constexpr int kChunkRows = 256;  // (token, head) rows of one chunk-kernel tile
 
 // Append cache-write table: one record per (sequence, page) the new tokens touch.

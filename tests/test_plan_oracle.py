@@ -29,39 +29,44 @@ def test_hand_derived_append_example():
     # L = [10, 100], C = [1, 70], Hkv = 2, G = 8 -> T = floor(256 / 8) = 32.
     # Single row 0: one page, W = 2, target = 4, chunk = 1, n = 1.
     # Chunk row 1: P = 30, tiles [0,32) [32,64) [64,70) with keys [0,62) [0,94) [0,100);
-    # costs 62*32 = 1984, 94*32 = 3008, 100*6 = 600; each KV-head group costs 5592 of a
-    # total 11184, so F = ceil(11184 / 8) = 1398 and each group is cut into
-    # n = min(3, ceil(5592 / 1398)) = 3 parts: tile i goes to part floor(S_i * 3 / 5592)
-    # with S = 0, 1984, 4992 -> parts 0, 1, 2, one tile each.  Parts by descending cost,
-    # ties (b, g, part): (1,0,1) (1,1,1) 3008, (1,0,0) (1,1,0) 1984, (1,0,2) (1,1,2) 600,
-    # dealt to the empty queues 0..5 in that order.
+    # costs in 64-key steps ceil(62/64) = 1, ceil(94/64) = 2, ceil(100/64) = 2; each
+    # KV-head group costs 5 of a total 10, so F = ceil(10 / 8) = 2 and each group is cut
+    # into n = min(3, ceil(5 / 2)) = 3 parts: tile i goes to part floor(S_i * 3 / 5) with
+    # S = 0, 1, 3 -> parts 0, 0, 1 (part 2 is empty and dropped).  Parts by descending
+    # cost, ties (b, g, part): (1,0,0) (1,1,0) cost 3, (1,0,1) (1,1,1) cost 2, dealt to the
+    # empty queues 0..3 in that order; queues 0 and 1 list the [32,64) tile (cost 2)
+    # before the [0,32) tile (cost 1).
     units, info = plan_ref([10, 100], [1, 70], 2, 8,
                            PlanParams(num_cus=4, units_per_cu=1, min_split_pages=1, max_splits=4))
     assert units == [
         (0, 0, 0, 10, 0, 1, 0, 1, -1, 0, 0, 9),
         (0, 1, 0, 10, 0, 1, 0, 1, -1, 0, 0, 9),
         (1, 0, 0, 94, 32, 64, 0, 1, -1, 1, 1, 30),
-        (1, 1, 0, 94, 32, 64, 0, 1, -1, 1, 1, 30),
         (1, 0, 0, 62, 0, 32, 0, 1, -1, 1, 1, 30),
+        (1, 1, 0, 94, 32, 64, 0, 1, -1, 1, 1, 30),
         (1, 1, 0, 62, 0, 32, 0, 1, -1, 1, 1, 30),
         (1, 0, 0, 100, 64, 70, 0, 1, -1, 1, 1, 30),
         (1, 1, 0, 100, 64, 70, 0, 1, -1, 1, 1, 30),
     ]
-    assert info["xcd_queue_lens"] == [1, 1, 1, 1, 1, 1, 0, 0]
+    assert info["xcd_queue_lens"] == [2, 2, 1, 1, 0, 0, 0, 0]
     assert info["n_single"] == 2 and info["n_chunk"] == 6 and info["q_tile"] == 32
 
 
 def test_hand_derived_group_parts():
-    # One 64-token chunk with no prior, Hkv = 1, G = 16 -> T = 16: four tiles with keys
-    # 16, 32, 48, 64 and costs 256, 512, 768, 1024 (total 2560, F = 320).  The group is cut
-    # into n = min(4, ceil(2560 / 320)) = 4 parts at floor(S_i * 4 / 2560), S = 0, 256,
-    # 768, 1536 -> parts 0, 0, 1, 2: {256, 512} = 768, {768}, {1024}.  Dealt by
-    # descending cost: part 2 (1024) -> queue 0, part 0 (768; ties by part index) ->
-    # queue 1, part 1 (768) -> queue 2; part 0 lists its tiles by descending cost.
-    units, info = plan_ref([64], [64], 1, 16, PlanParams())
+    # One 256-token chunk with no prior, Hkv = 1, G = 16 -> T = 16: tiles k = 0..15 with
+    # keys 16 (k + 1) and costs ceil((k + 1) / 4) = 1,1,1,1, 2,2,2,2, 3,3,3,3, 4,4,4,4
+    # (total 40, F = 5).  The group is cut into n = min(16, ceil(40 / 5)) = 8 parts at
+    # floor(S_k * 8 / 40), S = 0,1,2,3,4,6,8,10,12,15,18,21,24,28,32,36 -> parts
+    # 0,0,0,0,0, 1,1, 2,2, 3,3, 4,4, 5, 6, 7 of costs 6, 4, 5, 6, 7, 4, 4, 4.  By
+    # descending cost (ties by part index): p4 p0 p3 p2 p1 p5 p6 p7 -> queues 0..7.
+    # Each queue by descending cost, ties ascending q_begin: queue 0 = tiles 12, 11;
+    # queue 1 = tile 4 (cost 2), then tiles 0, 1, 2, 3; queue 2 = tiles 9, 10; queue 3 =
+    # tiles 8 (cost 3), 7 (cost 2); queue 4 = tiles 5, 6; queues 5-7 = tiles 13, 14, 15.
+    units, info = plan_ref([256], [256], 1, 16, PlanParams())
+    tile = lambda k: (0, 16 * (k + 1), 16 * k, 16 * (k + 1))
     assert [(u[2], u[3], u[4], u[5]) for u in units] == [
-        (0, 64, 48, 64), (0, 32, 16, 32), (0, 16, 0, 16), (0, 48, 32, 48)]
-    assert info["xcd_queue_lens"] == [1, 2, 1, 0, 0, 0, 0, 0]
+        tile(k) for k in (12, 11, 4, 0, 1, 2, 3, 9, 10, 8, 7, 5, 6, 13, 14, 15)]
+    assert info["xcd_queue_lens"] == [2, 5, 2, 2, 2, 1, 1, 1]
 
 
 def test_few_groups_fill_every_queue():
@@ -72,7 +77,7 @@ def test_few_groups_fill_every_queue():
     lens = info["xcd_queue_lens"]
     assert all(n > 0 for n in lens)
     chunks = units[info["n_single"]:]
-    cost = [(u[3] - u[2]) * (u[5] - u[4]) for u in chunks]
+    cost = [-(-(u[3] - u[2]) // 64) for u in chunks]
     qcost, pos = [], 0
     for n in lens:
         qcost.append(sum(cost[pos:pos + n]))
@@ -181,9 +186,9 @@ def check_invariants(seq_lens, q_lens, hkv, group, params):
         for c in range(S):
             kv = [u[3] - u[2] for u in singles[c::S]]
             assert kv == sorted(kv, reverse=True)
-    # chunk units: per-XCD queues, each (b, g) group contiguous inside one queue with its
-    # tiles by descending cost, groups dealt to the least-loaded queue
-    cost = lambda u: (u[3] - u[2]) * (u[5] - u[4])
+    # chunk units: per-XCD queues, each uncut (b, g) group inside one queue, every queue
+    # by descending cost (64-key steps), ties ascending (b, g, q_begin)
+    cost = lambda u: -(-(u[3] - u[2]) // 64)
     lens = info["xcd_queue_lens"]
     assert sum(lens) == len(chunks)
     seen = {}
@@ -201,12 +206,14 @@ def check_invariants(seq_lens, q_lens, hkv, group, params):
         for key, where in seen.items():
             gcost = sum(cost(u) for u in chunks if u[:2] == key)
             if gcost <= fair:
-                # an uncut group: one queue, contiguous, tiles by descending cost
+                # an uncut group: one queue
                 assert len({x for x, _ in where}) == 1
-                idx = sorted(i for _, i in where)
-                assert idx == list(range(idx[0], idx[0] + len(idx)))
-                c = [cost(chunks[i]) for i in idx]
-                assert c == sorted(c, reverse=True)
+        pos = 0
+        for n in lens:
+            q = chunks[pos:pos + n]
+            pos += n
+            keys = [(-cost(u), u[0], u[1], u[4]) for u in q]
+            assert keys == sorted(keys)
         # dealing bound: queues differ by at most one part, and a part costs at most
         # F plus one tile
         assert max(qcost) - min(qcost) <= fair + max(cost(u) for u in chunks)
