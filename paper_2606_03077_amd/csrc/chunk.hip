@@ -33,7 +33,9 @@
 // steps that reach past the tile's first token.  Row r = 32 w + column of the tile is
 // token q0 + r / G, head r % G; it sees keys k <= P_b + token.
 // Units arrive in per-XCD queues: workgroup w takes tile w / 8 of queue w % 8, so the
-// tiles of one (b, g), which read the same keys, run on one XCD and share its L2.
+// tiles of one (b, g), which read the same keys, run on one XCD and share its L2; each
+// queue holds its longest tiles first.  Wave priority is 1 through the first page pair of
+// a step and 0 through the second (see the note at the key loop).
 #include <cmath>
 #include <type_traits>
 
@@ -221,7 +223,6 @@ void chunk_kernel(ChunkArgs A) {
     s = a;
   };
 
-  // Causal / length mask and running-maximum update for step n.
   // Causal / length mask of step n; on the first step (exact) also the running maximum
   // (later steps check their probabilities instead, in pair()).
   auto prepare = [&](int key0, f32x16 (&s)[2], float& neg_m, bool exact) {
