@@ -84,12 +84,15 @@ def kernel_source_sha(kernel: str = "decode_kernel") -> str:
 
 
 def plan_sha(units: np.ndarray) -> str:
-    """Hash of the set of a plan's units: a kernel's traffic depends on which units run
-    (their pages, partials and tiles), not on their order, which the slot placement of a
-    one-wave plan sets from measured XCD weights that differ between devices."""
+    """Hash of a plan's units as far as a kernel's traffic depends on them: the set of
+    single (decode) units, whose order the slot placement sets from XCD weights measured on
+    the device, and the chunk tiles in their queue order, which is fixed by the lengths and
+    decides which tiles share an XCD's L2 at a time."""
     u = np.ascontiguousarray(units, dtype=np.int32).reshape(-1, 12)
-    u = u[np.lexsort(u.T[::-1])]
-    return hashlib.sha256(np.ascontiguousarray(u).tobytes()).hexdigest()[:16]
+    single = u[u[:, 10] == 0]
+    single = single[np.lexsort(single.T[::-1])]
+    chunk = u[u[:, 10] != 0]
+    return hashlib.sha256(np.ascontiguousarray(np.concatenate([single, chunk])).tobytes()).hexdigest()[:16]
 
 
 def counter_from_profile(kernel: str, workload: str, units_sha: str,

@@ -223,10 +223,12 @@ libra_status libra_kv_reshard_host(const void* const* src, int32_t n_src, int32_
  *    ceil(c / F)) parts, tile i (ascending q_begin) going to part floor(S_i n / c), S_i =
  *    cost of the group's earlier tiles; empty parts are dropped.  Parts by descending
  *    cost (ties ascending (b, g, part)) go to the queue with the least accumulated cost
- *    (ties to the lowest queue); each queue then lists its tiles by descending cost,
- *    ties ascending (b, g, q_begin); queue 0's tiles are listed first, then queue 1's,
- *    ... (the chunk launch runs queue x's tiles on workgroups w with w % 8 = x, so the
- *    tiles of a part share an L2, and each CU takes the longest tiles first).
+ *    (ties to the lowest queue); each queue then lists its parts by descending cost of
+ *    their longest tile (ties ascending (b, g, part)), a part's tiles together by
+ *    descending cost (ties ascending q_begin); queue 0's tiles are listed first, then
+ *    queue 1's, ... (the chunk launch runs queue x's tiles on workgroups w with
+ *    w % 8 = x, so the tiles of a part share an L2, and each CU takes the longest tiles
+ *    first).
  * 10. Single rows with n_b > 1 own n_b float32 partial-result slots per KV head,
  *    allotted in ascending (b, g): part_base(b, g) = earlier split rows' slots + g n_b.
  * 11. The single units are placed on S slots.  The decode launch dispatches workgroup w

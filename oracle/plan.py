@@ -48,8 +48,9 @@ units per CU, minimum split size in pages, maximum splits, chunk query tile).
    floor(S_i * n / c), S_i being the cost of the group's tiles before it; empty parts are
    dropped.  Parts, by descending cost (ties ascending (b, g, part)), are dealt to 8
    queues (one per XCD), each to the queue with the least accumulated cost (ties to the
-   lowest queue).  Each queue then lists its tiles by descending cost, ties ascending
-   (b, g, q_begin).
+   lowest queue).  Each queue then lists its parts by descending cost of their longest
+   tile (ties ascending (b, g, part)), a part's tiles together by descending cost (ties
+   ascending q_begin).
    The table lists all single units, then queue 0's tiles, queue 1's, ... queue 7's.
 10. Single rows with n_b > 1 own n_b partial-result slots per KV head, allotted in
     ascending (b, g) order: part_base(b, g) = (slots of earlier split rows) + g * n_b.
@@ -227,13 +228,17 @@ def plan_ref(seq_lens, q_lens, num_kv_heads: int, group: int, params: PlanParams
             parts.setdefault((b, g, before * n // c), []).append(u)
             before += cost(u)
     order = sorted(parts, key=lambda k: (-sum(cost(u) for u in parts[k]), k))
-    queues = [[] for _ in range(NUM_XCDS)]
+    qparts = [[] for _ in range(NUM_XCDS)]
     qcost = [0] * NUM_XCDS
     for k in order:
         x = min(range(NUM_XCDS), key=lambda i: (qcost[i], i))
         qcost[x] += sum(cost(u) for u in parts[k])
-        queues[x].extend(parts[k])
-    queues = [sorted(q, key=lambda u: (-cost(u), u[0], u[1], u[4])) for q in queues]
+        qparts[x].append(k)
+    tiles = {k: sorted(parts[k], key=lambda u: (-cost(u), u[4])) for k in parts}
+    queues = []
+    for ks in qparts:
+        ks = sorted(ks, key=lambda k: (-cost(tiles[k][0]), k))
+        queues.append([u for k in ks for u in tiles[k]])
     chunks = [u for q in queues for u in q]
 
     info = {"n_single": len(singles), "n_chunk": len(chunks), "n_partial_slots": slots,

@@ -206,10 +206,10 @@ libra_status build_plan(const libra_plan_desc& d, const int32_t* seq_lens, const
   // unless the group costs more than an eighth of the launch: it is then cut into
   // contiguous, cost-balanced parts so that every XCD gets work.  Parts by descending
   // cost (ties ascending (b, g, part)) are dealt to the XCD queue with the least
-  // accumulated cost (ties to the lowest queue); each queue then lists its tiles by
-  // descending cost, ties ascending (b, g, q_begin) (longest first, so the last tiles a
-  // CU takes are short; a group's tiles, of nearly equal cost, stay close); queues are
-  // listed one after another.  A tile costs its key-loop steps: the kernel spends the
+  // accumulated cost (ties to the lowest queue); each queue then lists its parts by
+  // descending cost of their longest tile, a part's tiles together and longest first (so
+  // the last tiles a CU takes are short, and the tiles that read the same keys run
+  // together); queues are listed one after another.  A tile costs its key-loop steps: the kernel spends the
   // same time on a step whatever the number of the tile's query tokens.
   auto cost = [](const Unit& u) { return ceil_div(u[U_KV1] - u[U_KV0], kChunkStepKeys); };
   int64_t total_cost = 0;
@@ -249,24 +249,41 @@ libra_status build_plan(const libra_plan_desc& d, const int32_t* seq_lens, const
     if (x.g != y.g) return x.g < y.g;
     return x.idx < y.idx;
   });
-  std::vector<std::vector<Unit>> queues(kNumXcds);
+  // Deal the parts; then each queue lists its parts by descending cost of their longest
+  // tile (ties ascending (b, g, part)), a part's tiles together, by descending cost (ties
+  // ascending q_begin).
+  std::vector<std::vector<size_t>> qparts(kNumXcds);
   int64_t qcost[kNumXcds] = {0};
   for (size_t k : porder) {
     int x = 0;
     for (int y = 1; y < kNumXcds; ++y)
       if (qcost[y] < qcost[x]) x = y;
     qcost[x] += parts[k].cost;
-    queues[x].insert(queues[x].end(), part_tiles.begin() + parts[k].first,
-                     part_tiles.begin() + parts[k].last);
+    qparts[x].push_back(k);
   }
-  for (auto& q : queues)
-    std::sort(q.begin(), q.end(), [&](const Unit& a, const Unit& b) {
-      const int64_t ca = cost(a), cb = cost(b);
-      if (ca != cb) return ca > cb;
-      if (a[U_B] != b[U_B]) return a[U_B] < b[U_B];
-      if (a[U_G] != b[U_G]) return a[U_G] < b[U_G];
-      return a[U_Q0] < b[U_Q0];
+  auto tile_order = [&](const Unit& a, const Unit& b) {
+    const int64_t ca = cost(a), cb = cost(b);
+    if (ca != cb) return ca > cb;
+    return a[U_Q0] < b[U_Q0];
+  };
+  std::vector<int64_t> longest_tile(parts.size(), 0);
+  for (size_t k = 0; k < parts.size(); ++k) {
+    std::sort(part_tiles.begin() + parts[k].first, part_tiles.begin() + parts[k].last, tile_order);
+    longest_tile[k] = cost(part_tiles[parts[k].first]);
+  }
+  std::vector<std::vector<Unit>> queues(kNumXcds);
+  for (int x = 0; x < kNumXcds; ++x) {
+    std::sort(qparts[x].begin(), qparts[x].end(), [&](size_t a, size_t b) {
+      if (longest_tile[a] != longest_tile[b]) return longest_tile[a] > longest_tile[b];
+      const Part &pa = parts[a], &pb = parts[b];
+      if (pa.b != pb.b) return pa.b < pb.b;
+      if (pa.g != pb.g) return pa.g < pb.g;
+      return pa.idx < pb.idx;
     });
+    for (size_t k : qparts[x])
+      queues[x].insert(queues[x].end(), part_tiles.begin() + parts[k].first,
+                       part_tiles.begin() + parts[k].last);
+  }
   chunks.clear();
   int32_t xcd_map[2 * kNumXcds];
   int32_t longest = 0;

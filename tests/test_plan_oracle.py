@@ -186,8 +186,8 @@ def check_invariants(seq_lens, q_lens, hkv, group, params):
         for c in range(S):
             kv = [u[3] - u[2] for u in singles[c::S]]
             assert kv == sorted(kv, reverse=True)
-    # chunk units: per-XCD queues, each uncut (b, g) group inside one queue, every queue
-    # by descending cost (64-key steps), ties ascending (b, g, q_begin)
+    # chunk units: per-XCD queues, each uncut (b, g) group inside one queue and contiguous
+    # in it, longest tiles of the queue's parts first (costs in 64-key steps)
     cost = lambda u: -(-(u[3] - u[2]) // 64)
     lens = info["xcd_queue_lens"]
     assert sum(lens) == len(chunks)
@@ -206,14 +206,20 @@ def check_invariants(seq_lens, q_lens, hkv, group, params):
         for key, where in seen.items():
             gcost = sum(cost(u) for u in chunks if u[:2] == key)
             if gcost <= fair:
-                # an uncut group: one queue
+                # an uncut group: one queue, contiguous, its tiles by descending cost
                 assert len({x for x, _ in where}) == 1
+                idx = sorted(i for _, i in where)
+                assert idx == list(range(idx[0], idx[0] + len(idx)))
+                c = [cost(chunks[i]) for i in idx]
+                assert c == sorted(c, reverse=True)
         pos = 0
         for n in lens:
             q = chunks[pos:pos + n]
             pos += n
-            keys = [(-cost(u), u[0], u[1], u[4]) for u in q]
-            assert keys == sorted(keys)
+            # runs of one (b, g): each run opens with its longest tile, and the runs open
+            # in non-increasing cost
+            heads = [cost(u) for i, u in enumerate(q) if i == 0 or q[i - 1][:2] != u[:2]]
+            assert heads == sorted(heads, reverse=True)
         # dealing bound: queues differ by at most one part, and a part costs at most
         # F plus one tile
         assert max(qcost) - min(qcost) <= fair + max(cost(u) for u in chunks)
