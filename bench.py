@@ -144,7 +144,8 @@ def cpu_baseline(batch, min_seconds: float = 10.0) -> dict:
     _ORACLE_BATCH = batch
     w = batch.workload
     visible = len(os.sched_getaffinity(0))
-    # a one-GPU machine allots this process a share of 16 host cores, whatever it shows
+    # at most 16 worker processes: the host cores one GPU's jobs may use, whatever the
+    # affinity mask shows
     workers = max(1, min(visible, 16))
     units = [(b, g) for b in range(len(batch.seq_lens)) for g in range(w.num_kv_heads)]
     order = np.random.default_rng(0).permutation(len(units))
@@ -174,7 +175,7 @@ def cpu_baseline(batch, min_seconds: float = 10.0) -> dict:
             "sample": f"{done_units} of {len(units)} (sequence, KV head) units of the "
                       f"{w.name} batch in seeded random order ({done_units / len(units):.2f} "
                       f"passes), {el:.1f} s, fp64 numpy {kind} oracle, one process per "
-                      f"core (the 16-core share of a one-GPU box; {visible} cores visible)",
+                      f"core ({workers} of {visible} visible cores, at most 16)",
             "kv_bytes": done_bytes}
 
 

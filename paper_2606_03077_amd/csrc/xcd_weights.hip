@@ -103,7 +103,7 @@ libra_status measure_hbm_read_rate(const void* buf, size_t bytes, int reps, doub
   // Completion-timed reads first: consecutive passes over a buffer larger than the
   // 256 MB MALL find none of their lines cached (each pass starts where the previous
   // one's surviving lines are not).  Then the fixed-interval reads.
-  for (int r = 0; e == hipSuccess && r <= reps; ++r) {  // round 0 warms up, not counted
+  for (int r = 0; e == hipSuccess && r <= reps; ++r) {  // pass 0 warms up, not counted
     e = hipEventRecord(a, s);
     if (e == hipSuccess) {
       hipLaunchKernelGGL(stream_read_kernel, dim3(kWorkgroups), dim3(kThreads), 0, s,
